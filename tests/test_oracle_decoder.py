@@ -1,0 +1,176 @@
+"""Pins for the oracle's decoder and verification rule (CPU only).
+
+* The full decoder is checked against torch's own pre-LN ``nn.TransformerDecoderLayer``
+  (a library implementation of self-attention, cross-attention and a GELU FFN) run in
+  float64 over the whole token sequence with a causal mask.  The oracle instead runs a
+  cached, block-at-a-time pass, so this also pins the KV-cache path.
+* Losslessness (section 3, "Speculative Loop"): one-pass verification returns the
+  target-greedy tokens.
+* Brute force: on a tiny vocabulary every possible draft block is verified.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from paper_2608_12703_amd import synth
+
+
+def _torch_reference_logits(cfg, params, enc, tokens):
+    """Library forward over the whole token sequence (positions 0..len-1)."""
+    d, H, F = cfg.d_model, cfg.n_heads, cfg.d_ffn
+    t = lambda name: torch.from_numpy(np.asarray(params[name], np.float64))
+    x = t("tok_emb")[torch.tensor(tokens)] + t("pos_emb")[: len(tokens)]
+    x = x[None]
+    mem = torch.from_numpy(np.asarray(enc, np.float64))[None]
+    causal = torch.nn.Transformer.generate_square_subsequent_mask(len(tokens), dtype=torch.float64)
+    for layer in range(cfg.n_layers):
+        p = lambda n: t(f"l{layer}.{n}")
+        mod = torch.nn.TransformerDecoderLayer(d, H, F, dropout=0.0, activation="gelu",
+                                               batch_first=True, norm_first=True,
+                                               dtype=torch.float64)
+        with torch.no_grad():
+            mod.self_attn.in_proj_weight.copy_(p("w_qkv"))
+            mod.self_attn.in_proj_bias.copy_(p("b_qkv"))
+            mod.self_attn.out_proj.weight.copy_(p("w_o"))
+            mod.self_attn.out_proj.bias.copy_(p("b_o"))
+            mod.multihead_attn.in_proj_weight.copy_(torch.cat([p("w_xq"), p("w_xkv")]))
+            mod.multihead_attn.in_proj_bias.copy_(torch.cat([p("b_xq"), p("b_xkv")]))
+            mod.multihead_attn.out_proj.weight.copy_(p("w_xo"))
+            mod.multihead_attn.out_proj.bias.copy_(p("b_xo"))
+            mod.linear1.weight.copy_(p("w_1")); mod.linear1.bias.copy_(p("b_1"))
+            mod.linear2.weight.copy_(p("w_2")); mod.linear2.bias.copy_(p("b_2"))
+            for i in (1, 2, 3):
+                getattr(mod, f"norm{i}").weight.copy_(p(f"ln{i}_g"))
+                getattr(mod, f"norm{i}").bias.copy_(p(f"ln{i}_b"))
+            mod.eval()
+            x = mod(x, mem, tgt_mask=causal, tgt_is_causal=True)
+    with torch.no_grad():
+        h = torch.nn.functional.layer_norm(x[0], (d,), t("lnf_g"), t("lnf_b"), eps=1e-5)
+        return (h @ t("tok_emb").T).numpy()
+
+
+@pytest.fixture(scope="module")
+def tiny(tiny_cfg):
+    cfg = tiny_cfg.with_(vocab=97)
+    params = synth.make_params(cfg)
+    enc = synth.make_encoder(cfg, 0, 37)
+    return cfg, params, enc
+
+
+def test_decoder_matches_torch_transformer_layers(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params, kv_dtype="f64")
+    cross = od.cross_kv(model, enc)
+    tokens = [5, 17, 3, 3, 96, 0, 41, 12, 8, 60]
+    ref = _torch_reference_logits(cfg, params, enc, tokens)
+    # (a) whole sequence as one block from an empty cache
+    st = od.new_state(model, cross, tokens[0])
+    out = od.forward_block(model, st, tokens)
+    np.testing.assert_allclose(out.logits, ref, rtol=0, atol=1e-11)
+    # (b) teacher-forced prefix committed through the cache, then the rest as a block
+    st = od.new_state(model, cross, tokens[0])
+    for i in range(6):                                 # feed tokens[0..5], one at a time
+        blk = od.forward_block(model, st, [st.t0])
+        np.testing.assert_allclose(blk.logits[0], ref[i], rtol=0, atol=1e-11)
+        st = od.commit(st, blk, 0, tokens[i + 1])
+    out = od.forward_block(model, st, tokens[6:])
+    np.testing.assert_allclose(out.logits, ref[6:], rtol=0, atol=1e-11)
+
+
+def test_cross_kv_is_plain_projection(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params, kv_dtype="f64")
+    cross = od.cross_kv(model, enc)
+    w = np.asarray(params["l1.w_xkv"], np.float64)
+    b = np.asarray(params["l1.b_xkv"], np.float64)
+    e = np.asarray(enc, np.float64)
+    d = cfg.d_model
+    # element (t, head 1, lane 5) of V by an explicit dot product
+    t, h, j = 11, 1, 5
+    col = d + h * 64 + j
+    assert abs(cross[1][1][t, h, j] - (np.dot(e[t], w[col]) + b[col])) < 1e-12
+    assert np.all(b[:d] == 0)          # keys carry no bias
+
+
+def _ar_tokens(model, state, n):
+    toks, margins, _ = od.ar_decode(model, state, n)
+    return toks, margins
+
+
+def test_verify_is_lossless_against_ar(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params)                  # bf16 caches, as on the GPU
+    cross = od.cross_kv(model, enc)
+    g = np.random.default_rng(0)
+    for trial in range(6):
+        n = int(g.integers(0, 20))
+        prefix = synth.make_prefix_kv(cfg, trial, n)
+        st = od.new_state(model, cross, int(g.integers(0, cfg.vocab)), prefix)
+        k = 5
+        y, _ = _ar_tokens(model, st, k + 1)
+        for G in range(0, k + 1):
+            drafts = synth.plant_drafts(np.array(y[:k]), G, g.integers(0, cfg.vocab - 1, k),
+                                        g.integers(0, cfg.vocab, k))
+            r = od.verify(model, st, drafts)
+            assert r.accepted == min(G, k)
+            assert r.emitted == y[: r.accepted + 1]
+            # committed state equals the AR state after the same number of tokens
+            _, _, st_ar = od.ar_decode(model, st, r.accepted + 1)
+            assert r.state.n == st_ar.n == st.n + r.accepted + 1
+            assert r.state.t0 == st_ar.t0
+            for (K1, V1), (K2, V2) in zip(r.state.self_kv, st_ar.self_kv):
+                np.testing.assert_allclose(K1, K2, rtol=2 ** -7, atol=1e-12)
+                np.testing.assert_allclose(V1, V2, rtol=2 ** -7, atol=1e-12)
+
+
+def test_brute_force_all_draft_blocks(tiny_cfg):
+    cfg = tiny_cfg.with_(n_layers=1, vocab=11)
+    params = synth.make_params(cfg)
+    model = od.Model(cfg, params)
+    cross = od.cross_kv(model, synth.make_encoder(cfg, 1, 9))
+    st = od.new_state(model, cross, 4, synth.make_prefix_kv(cfg, 1, 3))
+    k = 3
+    y, _ = _ar_tokens(model, st, k + 1)
+    for drafts in itertools.product(range(cfg.vocab), repeat=k):
+        r = od.verify(model, st, drafts)
+        expect = 0
+        while expect < k and drafts[expect] == y[expect]:
+            expect += 1
+        assert r.accepted == expect
+        assert r.emitted == y[: expect + 1]
+
+
+def test_rows_do_not_see_later_drafts(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params)
+    cross = od.cross_kv(model, enc)
+    st = od.new_state(model, cross, 3, synth.make_prefix_kv(cfg, 2, 7))
+    a = od.forward_block(model, st, [3, 10, 20, 30, 40])
+    b = od.forward_block(model, st, [3, 10, 20, 77, 1])
+    np.testing.assert_allclose(a.logits[:3], b.logits[:3], rtol=0, atol=1e-12)
+    assert np.abs(a.logits[3] - b.logits[3]).max() > 1e-6
+
+
+def test_spec_loop_with_heads_equals_ar(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params)
+    cross = od.cross_kv(model, enc)
+    heads = synth.make_draft_heads(cfg.with_(draft_heads=3))
+    st = od.new_state(model, cross, 1)
+    toks, accepts, _ = od.spec_decode_heads(model, st, heads, 24)
+    ar, _ = _ar_tokens(model, st, 24)
+    assert toks == ar
+    assert all(0 <= a <= 3 for a in accepts)
+
+
+def test_block_clamped_at_last_position(tiny):
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params)
+    cross = od.cross_kv(model, enc)
+    st = od.new_state(model, cross, 1, synth.make_prefix_kv(cfg.with_(n_layers=cfg.n_layers), 0, od.MAX_POS - 2))
+    od.forward_block(model, st, [1, 2])                 # positions 446, 447: allowed
+    with pytest.raises(ValueError):
+        od.forward_block(model, st, [1, 2, 3])          # position 448 does not exist
