@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Throughput of the batched speculative-verify step on one MI355X.
+
+Workload (default): the large-v3-shape bf16 decoder (32 layers, d 1280, 20 heads,
+FFN 5120, vocab 51866), batch 32, k = 6 drafts, 1500 encoder frames per sequence,
+committed KV lengths ~U{0..441}, drafts planted to agree with the target's greedy
+continuation for a Geometric(0.25) number of positions.  Inputs are seeded synthetic
+data (random-init N(0, 0.02) weights; no checkpoints or audio exist here).
+
+A step is one pass of the whole hot path over the batch: embed, 32 decoder layers over
+the paged self-KV cache and the encoder K/V, LM head + argmax, prefix accept, and the
+KV commit.  Each timed step starts from the same committed state (the commit's length
+update is undone by a 128-byte device copy after the step) so every step does the same
+work.  value = emitted tokens per step (accepted drafts + the bonus token, summed over
+the batch) / step time.
+
+Prints one JSON line (rank 0, N = 1 only: this build runs on one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--config", default="large_v3_bf16",
+                   choices=["large_v3_bf16", "small_bf16", "ragged_large_v3"])
+    p.add_argument("--layout", default="padded", choices=["padded", "packed"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-kernel-profile", action="store_true")
+    return p.parse_args()
+
+
+def gpu_greedy_continuation(sess, t0, ks):
+    """The target's own greedy tokens y_1..y_k per sequence, by repeated verification:
+    once d_1..d_i equal the greedy tokens, row i's argmax is the next one."""
+    B = len(t0)
+    drafts = [np.zeros(int(k), np.int64) for k in ks]
+    for it in range(int(max(ks))):
+        sess.step([np.concatenate([[t0[b]], drafts[b]]) for b in range(B)])
+        g = sess.results()["greedy"]
+        for b in range(B):
+            if it < ks[b]:
+                drafts[b][it] = g[sess.row_of(b, it)]
+    return drafts
+
+
+def cpu_baseline(cfg, params, wl, b=0):
+    """The oracle, untuned, on one sequence of the workload: one verify step of its k+1
+    rows (the encoder K/V prefill and the greedy continuation used to plant its drafts are
+    computed first and not timed, as on the GPU)."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import decoder as od
+    from paper_2608_12703_amd import synth
+    model = od.Model(cfg, params)
+    t0 = time.perf_counter()
+    cross = od.cross_kv(model, synth.make_encoder(cfg, b, int(wl.T[b])))
+    st = od.new_state(model, cross, int(wl.t0[b]), synth.make_prefix_kv(cfg, b, int(wl.n[b])))
+    k = int(wl.k[b])
+    y, _, _ = od.ar_decode(model, st, k)
+    d = synth.plant_drafts(np.array(y), int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])
+    setup = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    r = od.verify(model, st, d)
+    dt = time.perf_counter() - t1
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": (r.accepted + 1) / dt, "unit": "accepted tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"1 of {wl.batch} sequences (n={int(wl.n[b])}, k={k}, T={int(wl.T[b])}), one "
+                      f"verify step of {k + 1} rows: {r.accepted + 1} tokens in {dt:.2f} s "
+                      f"(encoder K/V prefill and draft planting, {setup:.1f} s, not timed)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs the verify step on one GPU; --gpus must be 1 "
+                                   "(data-parallel sharding over sequences is described in DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2608_12703_amd import ad, roofline, synth
+    from paper_2608_12703_amd.configs import CONFIGS
+    from paper_2608_12703_amd.harness import Session
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = CONFIGS[args.config]
+    layout = ad.AD_PADDED if args.layout == "padded" else ad.AD_PACKED
+    t_setup = time.perf_counter()
+    log(f"generating {cfg.name} inputs")
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    sess = Session(cfg, params, wl.batch, int(wl.k.max()), wl.T, layout=layout,
+                   packed_encoder=layout == ad.AD_PACKED)
+    log("encoder K/V prefill")
+    sess.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+    for b in range(wl.batch):
+        sess.import_prefix(b, synth.make_prefix_kv(cfg, b, int(wl.n[b])))
+    sess.set_kv_len(wl.n)
+    torch.cuda.synchronize()
+    log("planting drafts on the target's greedy continuation")
+    y = gpu_greedy_continuation(sess, wl.t0, wl.k)
+    blocks = [np.concatenate([[wl.t0[b]],
+                              synth.plant_drafts(y[b], int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])])
+              for b in range(wl.batch)]
+    sess.prepare(blocks)
+    kv0 = sess.kv_len.clone()
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup}, timed {args.steps}")
+
+    def one_step():
+        sess.run()
+        sess.commit()
+        sess.kv_len.copy_(kv0)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    res = sess.results()
+    assert res["err"] == 0, f"device error flag {res['err']}"
+    tokens = int(np.sum(res["accept_len"] + 1))
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        one_step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    res2 = sess.results()
+    assert np.array_equal(res2["accept_len"], res["accept_len"]), "steps were not repeatable"
+    log(f"{ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f}), {tokens} tokens/step")
+
+    sb = roofline.step_bytes(cfg, wl.n, wl.T, wl.k)
+    rows = sess.rows
+    roof = None
+    if not args.no_kernel_profile:
+        # the dominant kernel, timed with HIP events on the step's stream in a second pass
+        ad.profile_enable(sess.model, ad.PROF_CROSS_ATTN, cfg.n_layers * args.steps)
+        for _ in range(args.steps):
+            one_step()
+        tot, n_launch = ad.profile_read(sess.model)
+        ad.profile_enable(sess.model, ad.PROF_CROSS_ATTN, 0)
+        per_launch_s = tot / n_launch / 1e3
+        lb = roofline.cross_attn_launch_bytes(cfg, wl.T, rows)
+        achieved = lb / per_launch_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0, "unit": "GB/s",
+                "frac": round(achieved / 8000.0, 4), "traffic": None,
+                "kernel": "cross_attn", "launch_bytes": lb,
+                "launch_us": round(per_launch_s * 1e6, 2), "launches_timed": n_launch}
+        log(f"cross-attention: {per_launch_s * 1e6:.1f} us/launch, {achieved:.0f} GB/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("oracle CPU baseline (one sequence)")
+        cpu = cpu_baseline(cfg, params, wl)
+        log(f"oracle: {cpu['value']:.3f} tokens/s")
+
+    out = {
+        "metric": "accepted tokens/s, large-v3-shape spec-verify step (bf16); % of HBM roofline",
+        "value": round(tokens / (ms / 1e3), 1),
+        "unit": "accepted tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": wl.batch, "k": int(wl.k.max()),
+                   "frames": int(np.max(wl.T)), "layers": cfg.n_layers, "d_model": cfg.d_model,
+                   "layout": args.layout, "tokens_per_step": tokens, "rows": rows},
+        "step_hbm_bytes": sb["total"],
+        "step_hbm_frac": round(sb["total"] / (ms / 1e3) / roofline.HBM_PEAK, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,253 @@
+/*
+ * ad.h -- C-ABI of libad.so: the batched speculative-verify step for single-model
+ * speculative decoding of a Whisper-shape ASR decoder on MI355X (gfx950).
+ *
+ * Method (paper, section 3 "Speculative Loop"): in each round the target scores a
+ * drafted block [t0, d_1..d_k] in one decoder pass, takes its greedy token g_i at every
+ * block row and keeps the longest draft prefix with d_i = g_{i-1}; the round emits the
+ * a accepted drafts plus the target's own token g_a, so it advances 1 + a tokens
+ * (appendix "Cost derivation").  The accepted tokens and their cached keys/values feed
+ * the next round (appendix "Real cached loop").
+ *
+ * Conventions for every entry point:
+ *  - All pointers named "device" are HIP device pointers owned by the caller; the
+ *    library never allocates or frees device memory on the step path and never keeps a
+ *    pointer past the call (except the parameter views held by an ad_model).
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and is
+ *    asynchronous: nothing is synchronised and nothing is read back to the host.
+ *  - Validate-then-enqueue: host-detectable errors (NULL pointers, bad enums, sizes out
+ *    of range, workspace too small) return a negative ad_status and enqueue nothing.
+ *  - Device-detectable errors (a token id outside the vocabulary, a page index outside
+ *    the pool, a per-sequence length out of range, non-finite logits) OR a bit into
+ *    *err_flag; the affected sequence is skipped: its cache is not written and its
+ *    accept length is -1.  err_flag must be zeroed by the caller before a round.
+ *  - ad_last_error() returns a thread-local description of the last failure.
+ *  - Calls that overlap on one stream are ordered; calls on different streams that
+ *    share buffers race and are the caller's responsibility.
+ *
+ * Storage: dtype AD_F32 stores parameters, encoder states and caches in float32;
+ * AD_BF16 stores them in bfloat16.  Activations (the residual stream, LayerNorm,
+ * attention and GELU outputs, scores, logits) are float32 in both cases; bf16 matrix
+ * products accumulate in float32.
+ */
+#ifndef AD_H_
+#define AD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AD_OK = 0,
+  AD_EINVAL = -1,        /* NULL pointer, unknown enum, inconsistent descriptor      */
+  AD_ERANGE = -2,        /* a size outside its allowed range                        */
+  AD_ENOSPACE = -3,      /* workspace smaller than ad_workspace_size() requires      */
+  AD_EHIP = -4,          /* a HIP launch or runtime call failed                      */
+  AD_EUNSUPPORTED = -5   /* shape the kernels do not support (e.g. head width != 64) */
+} ad_status;
+
+typedef enum { AD_F32 = 0, AD_BF16 = 1 } ad_dtype;
+
+/* Row layout of a verify step.  PADDED: sequence b owns rows b*(k_max+1) ..
+ * b*(k_max+1)+k_max and rows past its own k_b are padding.  PACKED: sequence b owns
+ * rows cu_rows[b] .. cu_rows[b+1]-1 and cu_rows[b+1]-cu_rows[b] = k_b + 1. */
+typedef enum { AD_PADDED = 0, AD_PACKED = 1 } ad_layout;
+
+/* device-side error bits OR-ed into *err_flag */
+#define AD_ERR_LENGTH 1   /* k_b, n_b + k_b + 1 or packed row counts out of range */
+#define AD_ERR_PAGE 2     /* block-table entry outside [0, num_pages)              */
+#define AD_ERR_TOKEN 4    /* token id outside [0, vocab)                           */
+#define AD_ERR_FRAMES 8   /* T_b outside [1, max_frames] or past frames_cap        */
+#define AD_ERR_NONFINITE 16 /* NaN/Inf logits at a valid row                       */
+
+#define AD_HEAD_DIM 64    /* every attention head is 64 wide (score scale 1/8)     */
+#define AD_PAGE_TOKENS 16 /* tokens per self-KV page                               */
+
+typedef struct {
+  int32_t n_layers;   /* L                                                        */
+  int32_t d_model;    /* d = 64 * n_heads                                         */
+  int32_t n_heads;    /* H                                                        */
+  int32_t d_ffn;      /* F                                                        */
+  int32_t vocab;      /* V                                                        */
+  int32_t max_pos;    /* learned positions (448 for the Whisper shape)            */
+  int32_t max_frames; /* encoder frames per sequence (1500 for the Whisper shape) */
+  int32_t dtype;      /* ad_dtype                                                 */
+} ad_model_desc;
+
+typedef struct ad_model ad_model;
+
+/* Number of parameter pointers ad_model_create expects: 4 + 20 * n_layers. */
+int32_t ad_model_param_count(const ad_model_desc* desc);
+
+/*
+ * Create a model handle holding non-owning views of caller-allocated device parameters
+ * (all of the model dtype, row-major, matrices stored [out_features][in_features]).
+ * params[] order:
+ *   0 tok_emb [V][d] (also the tied LM head)   1 pos_emb [max_pos][d]
+ *   2 lnf_g [d]   3 lnf_b [d]
+ *   then per layer l, at 4 + 20 l:
+ *   +0 ln1_g [d]  +1 ln1_b [d]  +2 w_qkv [3d][d] (rows q | k | v)  +3 b_qkv [3d]
+ *   +4 w_o [d][d] +5 b_o [d]
+ *   +6 ln2_g [d]  +7 ln2_b [d]  +8 w_xq [d][d]  +9 b_xq [d]
+ *   +10 w_xkv [2d][d] (rows k | v) +11 b_xkv [2d]  +12 w_xo [d][d]  +13 b_xo [d]
+ *   +14 ln3_g [d] +15 ln3_b [d] +16 w_1 [F][d]  +17 b_1 [F]  +18 w_2 [d][F]  +19 b_2 [d]
+ * The decoder is pre-LN: x += SelfAttn(LN1 x); x += CrossAttn(LN2 x);
+ * x += W2 GELU(W1 LN3 x + b1) + b2; logits = LN_f(x) tok_emb^T (the paper's
+ * Whisper-large-v3 target, appendix "Whisper Cross-Architecture Check").
+ * Errors: AD_EINVAL (NULL, wrong n_params, bad dtype), AD_EUNSUPPORTED
+ * (d != 64 H, d or F not a multiple of 64), AD_ERANGE (non-positive sizes).
+ */
+ad_status ad_model_create(const ad_model_desc* desc, const void* const* params,
+                          int32_t n_params, ad_model** out);
+ad_status ad_model_destroy(ad_model* model);
+
+/*
+ * Paged self-attention KV cache.  pool holds
+ *   n_layers * 2 * num_pages * n_heads * 16 * 64 elements of the model dtype
+ * arranged as [layer][K|V][page][head][16-token tile]; the element order inside a tile
+ * is private to the library (write it only through ad_verify_step / ad_kv_import).
+ * Sequence b's position p lives in page block_table[b * pages_per_seq + p / 16].
+ */
+typedef struct {
+  void* pool;                 /* device                                              */
+  int32_t num_pages;
+  int32_t pages_per_seq;      /* row stride of block_table; >= ceil(max_pos / 16)   */
+  int32_t* kv_len;            /* device [B]: committed length n_b                    */
+  const int32_t* block_table; /* device [B][pages_per_seq]                           */
+} ad_kv;
+
+/*
+ * Encoder keys/values (the decoder's view of the frozen audio encoding, computed once
+ * per utterance by ad_cross_kv_prefill).  data holds
+ *   n_layers * 2 * n_heads * frames_cap * 64 elements of the model dtype
+ * arranged as [layer][K|V][head][frame slot], frames in 16-frame tiles (private order).
+ * Sequence b uses slots enc_off[b] .. enc_off[b] + enc_len[b] - 1; enc_off[b] must be
+ * a multiple of 16.  PADDED encoders use enc_off[b] = b * T_max, PACKED ones a running
+ * sum of T_b rounded up to 16; both give identical results.
+ */
+typedef struct {
+  void* data;                 /* device                                              */
+  int32_t frames_cap;         /* multiple of 16                                      */
+  const int32_t* enc_len;     /* device [B]: T_b                                     */
+  const int32_t* enc_off;     /* device [B]                                          */
+} ad_cross;
+
+typedef struct {
+  int32_t batch;              /* B >= 1                                              */
+  int32_t layout;             /* ad_layout                                           */
+  int32_t k_max;              /* max draft length, 0 <= k_max < max_pos              */
+  int32_t rows;               /* PADDED: B*(k_max+1); PACKED: sum_b (k_b + 1)        */
+  const int32_t* tokens;      /* device [rows]: per sequence t0, d_1 .. d_{k_b}      */
+  const int32_t* k;           /* device [B]: k_b in [0, k_max]                       */
+  const int32_t* cu_rows;     /* device [B+1] (PACKED only; NULL for PADDED)         */
+  ad_kv kv;
+  ad_cross cross;
+  int32_t* accept_len;        /* device [B] out: a_b, or -1 for a skipped sequence   */
+  int32_t* out_tokens;        /* device [B][k_max+1] out: g_0..g_{a_b}, then -1      */
+  int32_t* out_greedy;        /* device [rows] out (optional): g at every row        */
+  float* out_logits;          /* device [rows][vocab] out (optional)                 */
+  float* out_hidden;          /* device [rows][d] out (optional): LN_f output        */
+  float* out_margin;          /* device [rows] out (optional): top-1 minus top-2     */
+  int32_t* err_flag;          /* device [1]: AD_ERR_* bits are OR-ed in              */
+  void* workspace;            /* device scratch, >= ad_workspace_size() bytes        */
+  size_t workspace_bytes;
+} ad_step;
+
+/* Bytes of workspace a step with up to max_rows rows and max_batch sequences needs. */
+ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max_batch,
+                            size_t* bytes);
+
+/*
+ * Setup, once per utterance (not part of the per-round step): project encoder states
+ * into every layer's cross-attention keys and values,
+ *   K_l = enc W_xk,l^T,  V_l = enc W_xv,l^T + b_xv,l
+ * (the decoder reuses the encoded audio at every step; paper, section 1 and appendix
+ * "Draft architecture").  enc is device [frames_cap][d] of the model dtype, sequence b
+ * at rows enc_off[b].. (rows outside any sequence are projected too and never read).
+ * Errors: AD_EINVAL, AD_ERANGE (frames_cap not a positive multiple of 16).
+ */
+ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross,
+                              void* stream);
+
+/*
+ * The verify step (paper, section 3 "Speculative Loop"): embed the block of every
+ * sequence at positions n_b .. n_b + k_b, run the decoder over it with self-attention
+ * causal inside the block and over the committed cache, write the block's keys/values
+ * into the cache (write-through), take g_i = argmax of the float32 logits (lowest index
+ * on ties) at every row, accept a_b = max{ j <= k_b : d_i = g_{i-1} for all i <= j } and
+ * emit g_0..g_{a_b}.  kv_len is not changed; call ad_kv_commit next.
+ * Requires n_b + k_b + 1 <= max_pos, 1 <= T_b <= max_frames.
+ * Errors: AD_EINVAL, AD_ERANGE, AD_ENOSPACE, AD_EHIP (see conventions above).
+ */
+ad_status ad_verify_step(const ad_model* model, const ad_step* step, void* stream);
+
+/*
+ * Commit / roll back (appendix "Real cached loop"): kv_len[b] += accept_len[b] + 1 for
+ * every sequence with accept_len[b] >= 0.  Slots past the new length hold rejected
+ * drafts; they are never read and are overwritten by the next round.
+ */
+ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch, void* stream);
+
+/*
+ * Next draft block from linear draft heads on the final hidden state.  For sequence b
+ * take the LN_f output h at row row0_b + a_b (row0_b = first row of b in `layout`),
+ * d_i = argmax(W_i h) (float32 logits, lowest index on ties), i = 1..n_heads, and write
+ *   next_tokens[b][0] = out_tokens[b][a_b] (the bonus token, the next pending token)
+ *   next_tokens[b][i] = d_i
+ * heads_w is device [n_heads][vocab][d] of the model dtype.  hidden is the out_hidden
+ * of the step ([rows][d] float32).  Sequences with accept_len < 0 get -1 everywhere.
+ * Errors: AD_EINVAL, AD_ERANGE, AD_ENOSPACE.
+ */
+ad_status ad_draft_heads(const ad_model* model, const void* heads_w, int32_t n_heads,
+                         const float* hidden, int32_t layout, int32_t k_max,
+                         const int32_t* cu_rows, const int32_t* accept_len,
+                         const int32_t* out_tokens, int32_t batch, int32_t* next_tokens,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace ad_draft_heads needs for n_heads heads over `batch` sequences. */
+ad_status ad_draft_heads_workspace_size(const ad_model* model, int32_t n_heads, int32_t batch,
+                                        size_t* bytes);
+
+/*
+ * Import a committed prefix into the cache: src is device [L][2][n][H][64] (keys then
+ * values, model dtype, logical order) and becomes positions 0..n-1 of sequence b.
+ * Errors: AD_EINVAL, AD_ERANGE (n > pages_per_seq * 16 or n > max_pos);
+ * a page index outside the pool sets AD_ERR_PAGE and writes nothing.
+ */
+ad_status ad_kv_import(const ad_model* model, const ad_kv* kv, int32_t b, const void* src,
+                       int32_t n, int32_t* err_flag, void* stream);
+
+/*
+ * Export positions 0..n-1 of sequence b from the cache into dst, device
+ * [L][2][n][H][64] (the layout ad_kv_import reads): a snapshot of the decode state that
+ * a later ad_kv_import restores.  Errors as for ad_kv_import.
+ */
+ad_status ad_kv_export(const ad_model* model, const ad_kv* kv, int32_t b, void* dst,
+                       int32_t n, int32_t* err_flag, void* stream);
+
+/*
+ * Per-kernel timing with HIP events recorded on the step's stream.  After
+ * ad_profile_enable(model, kernel, max_launches), every launch of that kernel class made
+ * by ad_verify_step on this model is bracketed by a start/stop event pair (up to
+ * max_launches pairs; later launches are not timed).  ad_profile_read waits for the
+ * recorded events, returns the summed duration in milliseconds and the number of timed
+ * launches, and clears the record.  max_launches = 0 disables timing and frees the
+ * events.  Host-side state of the model handle: not thread-safe.
+ */
+#define AD_PROF_CROSS_ATTN 1  /* cross-attention over the encoder K/V              */
+#define AD_PROF_SELF_ATTN 2   /* self-attention over the paged cache               */
+#define AD_PROF_GEMM 3        /* the per-layer projections                         */
+#define AD_PROF_LM_HEAD 4     /* LM head with the fused argmax                     */
+ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches);
+ad_status ad_profile_read(ad_model* model, double* total_ms, int32_t* launches);
+
+/* Thread-local text of the last error (never NULL). */
+const char* ad_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AD_H_ */

@@ -183,6 +183,7 @@ class VerifyOut:
     logits: np.ndarray    # [k+1, V] float64
     hidden: np.ndarray    # [k+1, d]
     state: SeqState       # state after commit
+    block_kv: list        # per layer (K, V) written for all k+1 block rows, [k+1, H, 64]
 
 
 def decide(logits: np.ndarray):
@@ -204,7 +205,7 @@ def verify(model: Model, state: SeqState, drafts) -> VerifyOut:
     greedy, margins = decide(out.logits)
     a = accept_length(drafts, greedy)
     return VerifyOut(greedy, a, emitted_tokens(greedy, a), margins, out.logits, out.hidden,
-                     commit(state, out, a, greedy[a]))
+                     commit(state, out, a, greedy[a]), out.new_kv)
 
 
 def ar_step(model: Model, state: SeqState) -> VerifyOut:

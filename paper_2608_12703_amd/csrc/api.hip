@@ -1,0 +1,403 @@
+// C-ABI entry points of libad.so: argument validation, workspace layout and the order
+// of kernel launches that makes one verify step.
+#include <string>
+#include <vector>
+
+#include "../../include/ad.h"
+#include "common.h"
+#include "launch.h"
+
+struct ad_model {
+  ad_model_desc desc;
+  std::vector<const void*> p;
+  // launch timing (ad_profile_enable / ad_profile_read)
+  int prof_kernel = 0;
+  std::vector<hipEvent_t> prof_start, prof_stop;
+  int prof_used = 0;
+};
+
+namespace {
+
+thread_local std::string g_err = "";
+
+ad_status fail(ad_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+enum GlobalParam { P_TOK = 0, P_POS = 1, P_LNF_G = 2, P_LNF_B = 3 };
+enum LayerParam {
+  LN1_G, LN1_B, W_QKV, B_QKV, W_O, B_O, LN2_G, LN2_B, W_XQ, B_XQ, W_XKV, B_XKV, W_XO, B_XO,
+  LN3_G, LN3_B, W_1, B_1, W_2, B_2, N_LAYER_PARAMS
+};
+
+const void* lp(const ad_model* m, int layer, int which) {
+  return m->p[4 + layer * N_LAYER_PARAMS + which];
+}
+
+// Workspace carve-up for a step with M rows and B sequences.
+struct Workspace {
+  ad::SeqDesc* seqs;
+  ad::RowDesc* rows;
+  float* x;       // residual stream [M][d]
+  float* ln;      // LayerNorm output [M][d]
+  float* q;       // queries [M][d]
+  float* att;     // attention output [M][d]
+  float* hid;     // GELU output [M][F]
+  float* hidden;  // final LayerNorm output [M][d]
+  float* logits;  // [M][V]
+  int* greedy;    // [M]
+  size_t bytes;
+};
+
+Workspace carve(const ad_model_desc& d, int M, int B, char* base) {
+  Workspace w{};
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    char* p = base ? base + off : nullptr;
+    off += align256(n);
+    return p;
+  };
+  w.seqs = (ad::SeqDesc*)take(sizeof(ad::SeqDesc) * (size_t)B);
+  w.rows = (ad::RowDesc*)take(sizeof(ad::RowDesc) * (size_t)M);
+  w.x = (float*)take(4ull * M * d.d_model);
+  w.ln = (float*)take(4ull * M * d.d_model);
+  w.q = (float*)take(4ull * M * d.d_model);
+  w.att = (float*)take(4ull * M * d.d_model);
+  w.hid = (float*)take(4ull * M * d.d_ffn);
+  w.hidden = (float*)take(4ull * M * d.d_model);
+  w.logits = (float*)take(4ull * M * d.vocab);
+  w.greedy = (int*)take(4ull * M);
+  w.bytes = off;
+  return w;
+}
+
+ad_status check_hip(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(AD_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+  return AD_OK;
+}
+
+// Brackets one kernel launch with a profiling event pair when that class is enabled.
+struct ProfScope {
+  ad_model* m;
+  hipStream_t st;
+  int idx = -1;
+  ProfScope(const ad_model* model, int kernel, hipStream_t stream)
+      : m(const_cast<ad_model*>(model)), st(stream) {
+    if (m->prof_kernel == kernel && m->prof_used < (int)m->prof_start.size()) {
+      idx = m->prof_used++;
+      (void)hipEventRecord(m->prof_start[idx], st);
+    }
+  }
+  ~ProfScope() {
+    if (idx >= 0) (void)hipEventRecord(m->prof_stop[idx], st);
+  }
+};
+
+template <class S>
+void run_step(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
+  const ad_model_desc& D = m->desc;
+  const int M = s->rows, d = D.d_model, F = D.d_ffn, H = D.n_heads, V = D.vocab;
+  ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
+                 s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
+                 s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
+                 s->cross.frames_cap};
+  ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
+  ad::launch_embed<S>(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, st);
+
+  ad::EpiArgs e{};
+  e.rows = w.rows;
+  e.block_table = s->kv.block_table;
+  e.pages_per_seq = s->kv.pages_per_seq;
+  e.num_pages = s->kv.num_pages;
+  e.H = H;
+  e.d = d;
+  e.frames_cap = s->cross.frames_cap;
+  for (int l = 0; l < D.n_layers; ++l) {
+    e.layer = l;
+    // self-attention sublayer
+    ad::launch_layernorm<S>(M, d, w.x, lp(m, l, LN1_G), lp(m, l, LN1_B), w.ln, st);
+    e.out = w.q; e.ldo = d; e.cache = s->kv.pool;
+    ad::launch_gemm_valu<S>(ad::EPI_QKV, M, 3 * d, d, w.ln, lp(m, l, W_QKV), lp(m, l, B_QKV), e, st);
+    {
+      ProfScope ps(m, AD_PROF_SELF_ATTN, st);
+      ad::launch_self_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->kv.pool,
+                                   s->kv.num_pages, s->kv.block_table, s->kv.pages_per_seq, st);
+    }
+    e.out = w.x; e.ldo = d;
+    ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, d, w.att, lp(m, l, W_O), lp(m, l, B_O), e, st);
+    // cross-attention sublayer
+    ad::launch_layernorm<S>(M, d, w.x, lp(m, l, LN2_G), lp(m, l, LN2_B), w.ln, st);
+    e.out = w.q; e.ldo = d;
+    ad::launch_gemm_valu<S>(ad::EPI_STORE, M, d, d, w.ln, lp(m, l, W_XQ), lp(m, l, B_XQ), e, st);
+    {
+      ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
+      ad::launch_cross_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->cross.data,
+                                    s->cross.frames_cap, st);
+    }
+    e.out = w.x; e.ldo = d;
+    ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, d, w.att, lp(m, l, W_XO), lp(m, l, B_XO), e, st);
+    // feed-forward sublayer
+    ad::launch_layernorm<S>(M, d, w.x, lp(m, l, LN3_G), lp(m, l, LN3_B), w.ln, st);
+    e.out = w.hid; e.ldo = F;
+    ad::launch_gemm_valu<S>(ad::EPI_GELU, M, F, d, w.ln, lp(m, l, W_1), lp(m, l, B_1), e, st);
+    e.out = w.x; e.ldo = d;
+    ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, F, w.hid, lp(m, l, W_2), lp(m, l, B_2), e, st);
+  }
+  float* hidden = s->out_hidden ? s->out_hidden : w.hidden;
+  ad::launch_layernorm<S>(M, d, w.x, m->p[P_LNF_G], m->p[P_LNF_B], hidden, st);
+  float* logits = s->out_logits ? s->out_logits : w.logits;
+  e.out = logits; e.ldo = V;
+  {
+    ProfScope ps(m, AD_PROF_LM_HEAD, st);
+    ad::launch_gemm_valu<S>(ad::EPI_STORE, M, V, d, hidden, m->p[P_TOK], nullptr, e, st);
+  }
+  int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
+  ad::launch_argmax(M, V, logits, V, w.rows, greedy, s->out_margin, s->err_flag, st);
+  ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+}
+
+ad_status validate_desc(const ad_model_desc* d) {
+  if (!d) return fail(AD_EINVAL, "model descriptor is NULL");
+  if (d->dtype != AD_F32 && d->dtype != AD_BF16) return fail(AD_EINVAL, "unknown dtype");
+  if (d->n_layers <= 0 || d->d_model <= 0 || d->n_heads <= 0 || d->d_ffn <= 0 || d->vocab <= 1 ||
+      d->max_pos <= 0 || d->max_frames <= 0)
+    return fail(AD_ERANGE, "model sizes must be positive (vocab >= 2)");
+  if (d->d_model != AD_HEAD_DIM * d->n_heads)
+    return fail(AD_EUNSUPPORTED, "d_model must equal 64 * n_heads");
+  if (d->d_ffn % 64 != 0) return fail(AD_EUNSUPPORTED, "d_ffn must be a multiple of 64");
+  return AD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ad_last_error(void) { return g_err.c_str(); }
+
+int32_t ad_model_param_count(const ad_model_desc* desc) {
+  return desc ? 4 + N_LAYER_PARAMS * desc->n_layers : -1;
+}
+
+ad_status ad_model_create(const ad_model_desc* desc, const void* const* params, int32_t n_params,
+                          ad_model** out) {
+  if (!out) return fail(AD_EINVAL, "out is NULL");
+  *out = nullptr;
+  ad_status st = validate_desc(desc);
+  if (st != AD_OK) return st;
+  if (!params) return fail(AD_EINVAL, "params is NULL");
+  if (n_params != ad_model_param_count(desc))
+    return fail(AD_EINVAL, "expected " + std::to_string(ad_model_param_count(desc)) + " parameters");
+  for (int i = 0; i < n_params; ++i)
+    if (!params[i]) return fail(AD_EINVAL, "parameter " + std::to_string(i) + " is NULL");
+  ad_model* m = new ad_model;
+  m->desc = *desc;
+  m->p.assign(params, params + n_params);
+  *out = m;
+  return AD_OK;
+}
+
+static void prof_free(ad_model* m) {
+  for (auto e : m->prof_start) (void)hipEventDestroy(e);
+  for (auto e : m->prof_stop) (void)hipEventDestroy(e);
+  m->prof_start.clear();
+  m->prof_stop.clear();
+  m->prof_used = 0;
+  m->prof_kernel = 0;
+}
+
+ad_status ad_model_destroy(ad_model* model) {
+  if (model) prof_free(model);
+  delete model;
+  return AD_OK;
+}
+
+ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches) {
+  if (!model) return fail(AD_EINVAL, "model is NULL");
+  if (max_launches < 0 || max_launches > (1 << 20)) return fail(AD_ERANGE, "max_launches out of range");
+  if (max_launches > 0 && (kernel < AD_PROF_CROSS_ATTN || kernel > AD_PROF_LM_HEAD))
+    return fail(AD_EINVAL, "unknown kernel class");
+  prof_free(model);
+  if (max_launches == 0) return AD_OK;
+  model->prof_start.resize(max_launches);
+  model->prof_stop.resize(max_launches);
+  for (int i = 0; i < max_launches; ++i) {
+    if (hipEventCreate(&model->prof_start[i]) != hipSuccess ||
+        hipEventCreate(&model->prof_stop[i]) != hipSuccess) {
+      model->prof_start.resize(i);
+      model->prof_stop.resize(i);
+      prof_free(model);
+      return fail(AD_EHIP, "hipEventCreate failed");
+    }
+  }
+  model->prof_kernel = kernel;
+  return AD_OK;
+}
+
+ad_status ad_profile_read(ad_model* model, double* total_ms, int32_t* launches) {
+  if (!model || !total_ms || !launches) return fail(AD_EINVAL, "NULL argument");
+  double t = 0.0;
+  for (int i = 0; i < model->prof_used; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(model->prof_stop[i]) != hipSuccess ||
+        hipEventElapsedTime(&ms, model->prof_start[i], model->prof_stop[i]) != hipSuccess)
+      return fail(AD_EHIP, "reading profiling events failed");
+    t += ms;
+  }
+  *total_ms = t;
+  *launches = model->prof_used;
+  model->prof_used = 0;
+  return AD_OK;
+}
+
+ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max_batch, size_t* bytes) {
+  if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
+  if (max_rows <= 0 || max_batch <= 0) return fail(AD_ERANGE, "max_rows and max_batch must be positive");
+  *bytes = carve(model->desc, max_rows, max_batch, nullptr).bytes;
+  return AD_OK;
+}
+
+ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) {
+  if (!model || !s) return fail(AD_EINVAL, "model or step is NULL");
+  const ad_model_desc& D = model->desc;
+  if (!s->tokens || !s->k || !s->kv.pool || !s->kv.kv_len || !s->kv.block_table || !s->cross.data ||
+      !s->cross.enc_len || !s->cross.enc_off || !s->accept_len || !s->out_tokens || !s->err_flag ||
+      !s->workspace)
+    return fail(AD_EINVAL, "a required step pointer is NULL");
+  if (s->layout != AD_PADDED && s->layout != AD_PACKED) return fail(AD_EINVAL, "unknown layout");
+  if (s->layout == AD_PACKED && !s->cu_rows) return fail(AD_EINVAL, "packed layout needs cu_rows");
+  if (s->batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
+  if (s->k_max < 0 || s->k_max + 1 > D.max_pos) return fail(AD_ERANGE, "k_max out of range");
+  const long long full = (long long)s->batch * (s->k_max + 1);
+  if (s->layout == AD_PADDED && s->rows != full)
+    return fail(AD_ERANGE, "padded layout needs rows == batch * (k_max + 1)");
+  if (s->layout == AD_PACKED && (s->rows < s->batch || s->rows > full))
+    return fail(AD_ERANGE, "packed rows must lie in [batch, batch * (k_max + 1)]");
+  if (s->kv.num_pages < 1 || s->kv.pages_per_seq < 1) return fail(AD_ERANGE, "empty page pool");
+  if (s->cross.frames_cap < ad::kTile || s->cross.frames_cap % ad::kTile)
+    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 16");
+  const Workspace need = carve(D, s->rows, s->batch, nullptr);
+  if (s->workspace_bytes < need.bytes)
+    return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");
+  (void)hipGetLastError();
+  const Workspace w = carve(D, s->rows, s->batch, (char*)s->workspace);
+  hipStream_t st = (hipStream_t)stream;
+  if (D.dtype == AD_BF16) run_step<ad::BF16>(model, s, w, st);
+  else run_step<ad::F32>(model, s, w, st);
+  return check_hip("ad_verify_step");
+}
+
+ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch, void* stream) {
+  if (!kv_len || !accept_len) return fail(AD_EINVAL, "NULL argument");
+  if (batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
+  (void)hipGetLastError();
+  ad::launch_commit(batch, kv_len, accept_len, (hipStream_t)stream);
+  return check_hip("ad_kv_commit");
+}
+
+ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross, void* stream) {
+  if (!model || !enc || !cross || !cross->data) return fail(AD_EINVAL, "NULL argument");
+  if (cross->frames_cap < ad::kTile || cross->frames_cap % ad::kTile)
+    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 16");
+  const ad_model_desc& D = model->desc;
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  ad::EpiArgs e{};
+  e.cache = cross->data;
+  e.H = D.n_heads;
+  e.d = D.d_model;
+  e.frames_cap = cross->frames_cap;
+  // The float32 A operand of the VALU product: widen the encoder states once.
+  for (int l = 0; l < D.n_layers; ++l) {
+    e.layer = l;
+    if (D.dtype == AD_BF16)
+      ad::launch_gemm_valu_bf16a(ad::EPI_XKV, cross->frames_cap, 2 * D.d_model, D.d_model, enc,
+                                 lp(model, l, W_XKV), lp(model, l, B_XKV), e, st);
+    else
+      ad::launch_gemm_valu<ad::F32>(ad::EPI_XKV, cross->frames_cap, 2 * D.d_model, D.d_model,
+                                    (const float*)enc, lp(model, l, W_XKV), lp(model, l, B_XKV), e, st);
+  }
+  return check_hip("ad_cross_kv_prefill");
+}
+
+ad_status ad_draft_heads_workspace_size(const ad_model* model, int32_t n_heads, int32_t batch,
+                                        size_t* bytes) {
+  if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
+  if (n_heads < 1 || batch < 1) return fail(AD_ERANGE, "n_heads and batch must be positive");
+  const ad_model_desc& D = model->desc;
+  *bytes = align256(4ull * batch * D.d_model) + align256(4ull * n_heads * batch * D.vocab) +
+           align256(4ull * n_heads * batch);
+  return AD_OK;
+}
+
+ad_status ad_draft_heads(const ad_model* model, const void* heads_w, int32_t n_heads, const float* hidden,
+                         int32_t layout, int32_t k_max, const int32_t* cu_rows, const int32_t* accept_len,
+                         const int32_t* out_tokens, int32_t batch, int32_t* next_tokens, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (!model || !heads_w || !hidden || !accept_len || !out_tokens || !next_tokens || !workspace)
+    return fail(AD_EINVAL, "NULL argument");
+  if (layout != AD_PADDED && layout != AD_PACKED) return fail(AD_EINVAL, "unknown layout");
+  if (layout == AD_PACKED && !cu_rows) return fail(AD_EINVAL, "packed layout needs cu_rows");
+  if (n_heads < 1 || batch < 1 || k_max < 0) return fail(AD_ERANGE, "sizes out of range");
+  size_t need = 0;
+  ad_draft_heads_workspace_size(model, n_heads, batch, &need);
+  if (workspace_bytes < need) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need) + " bytes");
+  const ad_model_desc& D = model->desc;
+  char* base = (char*)workspace;
+  float* hsel = (float*)base;
+  base += align256(4ull * batch * D.d_model);
+  float* logits = (float*)base;
+  base += align256(4ull * n_heads * batch * D.vocab);
+  int* greedy = (int*)base;
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  ad::launch_gather_hidden(batch, D.d_model, layout, k_max, cu_rows, accept_len, hidden, hsel, st);
+  const size_t esz = D.dtype == AD_BF16 ? 2 : 4;
+  ad::EpiArgs e{};
+  for (int i = 0; i < n_heads; ++i) {
+    e.out = logits + (size_t)i * batch * D.vocab;
+    e.ldo = D.vocab;
+    const void* w = (const char*)heads_w + (size_t)i * D.vocab * D.d_model * esz;
+    if (D.dtype == AD_BF16)
+      ad::launch_gemm_valu<ad::BF16>(ad::EPI_STORE, batch, D.vocab, D.d_model, hsel, w, nullptr, e, st);
+    else
+      ad::launch_gemm_valu<ad::F32>(ad::EPI_STORE, batch, D.vocab, D.d_model, hsel, w, nullptr, e, st);
+  }
+  // the err flag of the step is not touched here: non-finite head logits give -1 drafts
+  ad::launch_argmax(n_heads * batch, D.vocab, logits, D.vocab, nullptr, greedy, nullptr, nullptr, st);
+  ad::launch_assemble_next(batch, n_heads, k_max, accept_len, out_tokens, greedy, next_tokens, st);
+  return check_hip("ad_draft_heads");
+}
+
+static ad_status kv_copy(const char* what, bool to_linear, const ad_model* model, const ad_kv* kv,
+                         int32_t b, void* lin, int32_t n, int32_t* err_flag, void* stream) {
+  if (!model || !kv || !kv->pool || !kv->block_table || !err_flag || (n > 0 && !lin))
+    return fail(AD_EINVAL, std::string(what) + ": NULL argument");
+  const ad_model_desc& D = model->desc;
+  if (b < 0 || n < 0 || n > D.max_pos || n > kv->pages_per_seq * ad::kTile)
+    return fail(AD_ERANGE, std::string(what) + ": sequence index or prefix length out of range");
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  if (D.dtype == AD_BF16)
+    ad::launch_kv_copy<ad::BF16>(to_linear, D.n_layers, D.n_heads, n, b, lin, kv->pool, kv->num_pages,
+                                 kv->block_table, kv->pages_per_seq, err_flag, st);
+  else
+    ad::launch_kv_copy<ad::F32>(to_linear, D.n_layers, D.n_heads, n, b, lin, kv->pool, kv->num_pages,
+                                kv->block_table, kv->pages_per_seq, err_flag, st);
+  return check_hip(what);
+}
+
+ad_status ad_kv_import(const ad_model* model, const ad_kv* kv, int32_t b, const void* src, int32_t n,
+                       int32_t* err_flag, void* stream) {
+  return kv_copy("ad_kv_import", false, model, kv, b, const_cast<void*>(src), n, err_flag, stream);
+}
+
+ad_status ad_kv_export(const ad_model* model, const ad_kv* kv, int32_t b, void* dst, int32_t n,
+                       int32_t* err_flag, void* stream) {
+  return kv_copy("ad_kv_export", true, model, kv, b, dst, n, err_flag, stream);
+}
+
+}  // extern "C"

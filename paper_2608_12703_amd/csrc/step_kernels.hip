@@ -1,0 +1,314 @@
+// Small kernels of the verify step: descriptor preparation and validation, embedding,
+// LayerNorm, argmax with top-2 margin, the prefix-accept scan, commit, prefix import and
+// the draft-head helpers.
+#include "common.h"
+#include "launch.h"
+
+namespace ad {
+
+// ---------------------------------------------------------------- descriptors
+
+__global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
+  for (int b = threadIdx.x + blockIdx.x * blockDim.x; b < a.B; b += blockDim.x * gridDim.x) {
+    const int kb = a.k[b];
+    const int n = a.kv_len[b];
+    const int T = a.enc_len[b];
+    const int off = a.enc_off[b];
+    int row0 = a.layout == 0 ? b * (a.k_max + 1) : a.cu_rows[b];
+    int e = 0;
+    if (kb < 0 || kb > a.k_max || n < 0 || n + kb + 1 > a.max_pos) e |= 1;
+    if (a.layout == 1) {
+      const int r1 = a.cu_rows[b + 1];
+      if (row0 < 0 || r1 > a.rows || r1 - row0 != kb + 1) e |= 1;
+    }
+    if (T < 1 || T > a.max_frames || off < 0 || (off & (kTile - 1)) || off + T > a.frames_cap)
+      e |= 8;
+    if (!(e & 1)) {
+      const int last_page = (n + kb) / kTile;
+      if (last_page >= a.pages_per_seq) {
+        e |= 2;
+      } else {
+        for (int p = 0; p <= last_page; ++p) {
+          const int pg = a.block_table[(size_t)b * a.pages_per_seq + p];
+          if (pg < 0 || pg >= a.num_pages) e |= 2;
+        }
+      }
+      for (int i = 0; i <= kb; ++i) {
+        const int t = a.tokens[row0 + i];
+        if (t < 0 || t >= a.V) e |= 4;
+      }
+    }
+    if (e) atomicOr(err, e);
+    if (e & 1) row0 = 0;
+    seqs[b] = SeqDesc{row0, e ? 0 : kb, e ? 0 : n, e ? 1 : T, e ? 0 : off, e == 0, 0, 0};
+  }
+}
+
+__global__ void prep_row_kernel(StepArgs a, const SeqDesc* seqs, RowDesc* rows) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= a.rows) return;
+  int b, i;
+  if (a.layout == 0) {
+    b = m / (a.k_max + 1);
+    i = m % (a.k_max + 1);
+  } else {
+    // last sequence whose first row is <= m (bounded binary search over cu_rows)
+    int lo = 0, hi = a.B - 1;
+    b = -1;
+    while (lo <= hi) {
+      const int mid = (lo + hi) >> 1;
+      if (a.cu_rows[mid] <= m) { b = mid; lo = mid + 1; } else { hi = mid - 1; }
+    }
+    i = b >= 0 ? m - a.cu_rows[b] : 0;
+  }
+  RowDesc r{-1, 0, 0, 0};
+  if (b >= 0 && b < a.B) {
+    const SeqDesc s = seqs[b];
+    if (s.valid && i >= 0 && i <= s.k && s.row0 + i == m) {
+      r.seq = b;
+      r.i = i;
+      r.pos = s.n + i;
+      r.token = a.tokens[m];
+    }
+  }
+  rows[m] = r;
+}
+
+// ---------------------------------------------------------------- embedding
+
+template <class S>
+__global__ void embed_kernel(int d, const RowDesc* rows, const typename S::T* tok_emb,
+                             const typename S::T* pos_emb, float* x) {
+  const int m = blockIdx.x;
+  const RowDesc r = rows[m];
+  for (int j = threadIdx.x; j < d; j += blockDim.x)
+    x[(size_t)m * d + j] = S::ld(tok_emb, (size_t)r.token * d + j) + S::ld(pos_emb, (size_t)r.pos * d + j);
+}
+
+// ---------------------------------------------------------------- LayerNorm
+// out = (x - mean) / sqrt(var + 1e-5) * g + b, biased variance, two passes over the row.
+
+template <class S>
+__global__ void __launch_bounds__(256) layernorm_kernel(int d, const float* x,
+                                                        const typename S::T* g,
+                                                        const typename S::T* b, float* out) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const float* xr = x + (size_t)m * d;
+  float s = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) s += xr[j];
+  const float mean = block_sum<4>(s, red) / (float)d;
+  float v = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float t = xr[j] - mean;
+    v += t * t;
+  }
+  const float var = block_sum<4>(v, red) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + 1e-5f);
+  for (int j = threadIdx.x; j < d; j += 256)
+    out[(size_t)m * d + j] = (xr[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j);
+}
+
+// ---------------------------------------------------------------- argmax + margin
+// Per row: largest logit (lowest index on ties) and the runner-up value.
+
+struct Top2 {
+  float v1;
+  int i1;
+  float v2;
+};
+__device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
+  const bool a_wins = (a.v1 > b.v1) || (a.v1 == b.v1 && a.i1 < b.i1);
+  Top2 r;
+  if (a_wins) { r.v1 = a.v1; r.i1 = a.i1; r.v2 = fmaxf(a.v2, b.v1); }
+  else        { r.v1 = b.v1; r.i1 = b.i1; r.v2 = fmaxf(b.v2, a.v1); }
+  return r;
+}
+
+__global__ void __launch_bounds__(256) argmax_kernel(int V, const float* logits, size_t ld,
+                                                     const RowDesc* rows, int* greedy,
+                                                     float* margin, int* err) {
+  __shared__ Top2 red[4];
+  __shared__ int bad_s;
+  const int m = blockIdx.x;
+  const float* lr = logits + (size_t)m * ld;
+  if (threadIdx.x == 0) bad_s = 0;
+  __syncthreads();
+  Top2 t{-INFINITY, 0x7fffffff, -INFINITY};
+  int bad = 0;
+  for (int j = threadIdx.x; j < V; j += 256) {
+    const float v = lr[j];
+    if (!isfinite(v)) { bad = 1; continue; }
+    if (v > t.v1) { t.v2 = t.v1; t.v1 = v; t.i1 = j; }
+    else if (v > t.v2) { t.v2 = v; }
+  }
+  if (bad) atomicOr(&bad_s, 1);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    Top2 u;
+    u.v1 = __shfl_xor(t.v1, o, kWave);
+    u.i1 = __shfl_xor(t.i1, o, kWave);
+    u.v2 = __shfl_xor(t.v2, o, kWave);
+    t = top2_merge(t, u);
+  }
+  const int w = threadIdx.x / kWave;
+  if (threadIdx.x % kWave == 0) red[w] = t;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    Top2 r = red[0];
+    for (int i = 1; i < 4; ++i) r = top2_merge(r, red[i]);
+    const bool valid_row = rows ? rows[m].seq >= 0 : true;
+    if (bad_s && valid_row && err) atomicOr(err, 16);
+    greedy[m] = (bad_s && valid_row) ? -1 : r.i1;
+    if (margin) margin[m] = r.v1 - r.v2;
+  }
+}
+
+// ---------------------------------------------------------------- accept / commit
+
+__global__ void accept_kernel(int B, int k_max, const SeqDesc* seqs, const int* tokens,
+                              const int* greedy, int* accept_len, int* out_tokens) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const SeqDesc s = seqs[b];
+  int a = -1;
+  if (s.valid) {
+    bool ok = true;
+    for (int i = 0; i <= s.k; ++i) ok = ok && greedy[s.row0 + i] >= 0;
+    if (ok) {
+      a = 0;
+      while (a < s.k && tokens[s.row0 + 1 + a] == greedy[s.row0 + a]) ++a;
+    }
+  }
+  accept_len[b] = a;
+  for (int i = 0; i <= k_max; ++i)
+    out_tokens[(size_t)b * (k_max + 1) + i] = (a >= 0 && i <= a) ? greedy[s.row0 + i] : -1;
+}
+
+__global__ void commit_kernel(int B, int* kv_len, const int* accept_len) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int a = accept_len[b];
+  if (a >= 0) kv_len[b] += a + 1;
+}
+
+// ---------------------------------------------------------------- prefix import
+
+// EXPORT = false: src [L][2][n][H][64] -> pool; EXPORT = true: pool -> dst.
+template <class S, bool EXPORT>
+__global__ void kv_copy_kernel(int L, int H, int n, int b, typename S::T* lin,
+                               typename S::T* pool, int num_pages, const int* block_table,
+                               int pages_per_seq, int* err) {
+  // one thread per element of the logical array [L][2][n][H][64]
+  const size_t total = (size_t)L * 2 * n * H * kHead;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  size_t r = idx;
+  const int j = r % kHead; r /= kHead;
+  const int h = r % H; r /= H;
+  const int p = r % n; r /= n;
+  const int kv = r % 2; r /= 2;
+  const int layer = (int)r;
+  const int pg = block_table[(size_t)b * pages_per_seq + p / kTile];
+  if (pg < 0 || pg >= num_pages) {
+    atomicOr(err, 2);
+    return;
+  }
+  const size_t at = kv_tile_base(layer, kv, pg, h, num_pages, H) + tile_off(p % kTile, j);
+  if (EXPORT) lin[idx] = pool[at];
+  else pool[at] = lin[idx];
+}
+
+// ---------------------------------------------------------------- draft heads
+
+__global__ void gather_hidden_kernel(int B, int d, int layout, int k_max, const int* cu_rows,
+                                     const int* accept_len, const float* hidden, float* hsel) {
+  const int b = blockIdx.x;
+  const int a = accept_len[b];
+  const int row0 = layout == 0 ? b * (k_max + 1) : cu_rows[b];
+  for (int j = threadIdx.x; j < d; j += blockDim.x)
+    hsel[(size_t)b * d + j] = a >= 0 ? hidden[(size_t)(row0 + a) * d + j] : 0.f;
+}
+
+__global__ void assemble_next_kernel(int B, int n_heads, int k_max, const int* accept_len,
+                                     const int* out_tokens, const int* head_greedy,
+                                     int* next_tokens) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int a = accept_len[b];
+  int* nt = next_tokens + (size_t)b * (n_heads + 1);
+  nt[0] = a >= 0 ? out_tokens[(size_t)b * (k_max + 1) + a] : -1;
+  for (int i = 0; i < n_heads; ++i) nt[1 + i] = a >= 0 ? head_greedy[(size_t)i * B + b] : -1;
+}
+
+// ---------------------------------------------------------------- launchers
+
+void launch_prep(const StepArgs& a, SeqDesc* seqs, RowDesc* rows, int* err, hipStream_t st) {
+  hipLaunchKernelGGL(prep_seq_kernel, dim3((a.B + 255) / 256), dim3(256), 0, st, a, seqs, err);
+  hipLaunchKernelGGL(prep_row_kernel, dim3((a.rows + 255) / 256), dim3(256), 0, st, a, seqs, rows);
+}
+
+template <class S>
+void launch_embed(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
+                  hipStream_t st) {
+  hipLaunchKernelGGL(embed_kernel<S>, dim3(M), dim3(256), 0, st, d, rows,
+                     (const typename S::T*)tok, (const typename S::T*)pos, x);
+}
+template void launch_embed<F32>(int, int, const RowDesc*, const void*, const void*, float*, hipStream_t);
+template void launch_embed<BF16>(int, int, const RowDesc*, const void*, const void*, float*, hipStream_t);
+
+template <class S>
+void launch_layernorm(int M, int d, const float* x, const void* g, const void* b, float* out,
+                      hipStream_t st) {
+  hipLaunchKernelGGL(layernorm_kernel<S>, dim3(M), dim3(256), 0, st, d, x,
+                     (const typename S::T*)g, (const typename S::T*)b, out);
+}
+template void launch_layernorm<F32>(int, int, const float*, const void*, const void*, float*, hipStream_t);
+template void launch_layernorm<BF16>(int, int, const float*, const void*, const void*, float*, hipStream_t);
+
+void launch_argmax(int M, int V, const float* logits, size_t ld, const RowDesc* rows, int* greedy,
+                   float* margin, int* err, hipStream_t st) {
+  hipLaunchKernelGGL(argmax_kernel, dim3(M), dim3(256), 0, st, V, logits, ld, rows, greedy, margin, err);
+}
+
+void launch_accept(int B, int k_max, const SeqDesc* seqs, const int* tokens, const int* greedy,
+                   int* accept_len, int* out_tokens, hipStream_t st) {
+  hipLaunchKernelGGL(accept_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, k_max, seqs, tokens,
+                     greedy, accept_len, out_tokens);
+}
+
+void launch_commit(int B, int* kv_len, const int* accept_len, hipStream_t st) {
+  hipLaunchKernelGGL(commit_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, kv_len, accept_len);
+}
+
+template <class S>
+void launch_kv_copy(bool to_linear, int L, int H, int n, int b, void* lin, void* pool, int num_pages,
+                    const int* block_table, int pages_per_seq, int* err, hipStream_t st) {
+  const size_t total = (size_t)L * 2 * n * H * kHead;
+  if (total == 0) return;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (to_linear)
+    hipLaunchKernelGGL((kv_copy_kernel<S, true>), grid, dim3(256), 0, st, L, H, n, b,
+                       (typename S::T*)lin, (typename S::T*)pool, num_pages, block_table,
+                       pages_per_seq, err);
+  else
+    hipLaunchKernelGGL((kv_copy_kernel<S, false>), grid, dim3(256), 0, st, L, H, n, b,
+                       (typename S::T*)lin, (typename S::T*)pool, num_pages, block_table,
+                       pages_per_seq, err);
+}
+template void launch_kv_copy<F32>(bool, int, int, int, int, void*, void*, int, const int*, int, int*, hipStream_t);
+template void launch_kv_copy<BF16>(bool, int, int, int, int, void*, void*, int, const int*, int, int*, hipStream_t);
+
+void launch_gather_hidden(int B, int d, int layout, int k_max, const int* cu_rows,
+                          const int* accept_len, const float* hidden, float* hsel, hipStream_t st) {
+  hipLaunchKernelGGL(gather_hidden_kernel, dim3(B), dim3(256), 0, st, B, d, layout, k_max, cu_rows,
+                     accept_len, hidden, hsel);
+}
+
+void launch_assemble_next(int B, int n_heads, int k_max, const int* accept_len, const int* out_tokens,
+                          const int* head_greedy, int* next_tokens, hipStream_t st) {
+  hipLaunchKernelGGL(assemble_next_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, n_heads, k_max,
+                     accept_len, out_tokens, head_greedy, next_tokens);
+}
+
+}  // namespace ad

@@ -1,0 +1,115 @@
+"""Shared pieces of the GPU parity tests: build a device session and the matching oracle
+states from the same seeded inputs, and compare outputs.
+
+The parity bar: accept lengths, emitted tokens and KV lengths bit-exact, except at
+positions whose oracle top-2 logit margin is below 1e-3; logits within 2e-2 (bf16
+storage) or 1e-4 (float32 storage).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import decoder as od
+from paper_2608_12703_amd import ad, synth
+from paper_2608_12703_amd.harness import Session
+
+MARGIN_EXCLUDE = 1e-3
+LOGIT_TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def oracle_model(cfg, params):
+    return od.Model(cfg, params)
+
+
+def oracle_state(cfg, model, b, n, T, t0):
+    cross = od.cross_kv(model, synth.make_encoder(cfg, b, T))
+    return od.new_state(model, cross, t0, synth.make_prefix_kv(cfg, b, n))
+
+
+def subset(wl, ids):
+    """The workload of the listed sequences only (their own seeded inputs)."""
+    ids = list(ids)
+    return synth.StepWorkload(wl.k[ids], wl.n[ids], wl.T[ids], wl.t0[ids], wl.G[ids],
+                              [wl.fill_ne[i] for i in ids], [wl.fill_any[i] for i in ids])
+
+
+def device_session(cfg, params, wl, *, layout=ad.AD_PADDED, packed_encoder=False,
+                   want_logits=True, poison=False, k_max=None, seq_ids=None):
+    """Device state for workload `wl`; sequence b draws the inputs of seq_ids[b]."""
+    k_max = int(wl.k.max()) if k_max is None else k_max
+    ids = list(range(wl.batch)) if seq_ids is None else list(seq_ids)
+    s = Session(cfg, params, wl.batch, k_max, wl.T, layout=layout,
+                packed_encoder=packed_encoder, want_logits=want_logits)
+    if poison:
+        s.pool.fill_(float("nan"))
+        s.cross.fill_(float("nan"))
+    s.prefill_encoder([synth.make_encoder(cfg, ids[b], int(wl.T[b])) for b in range(wl.batch)])
+    for b in range(wl.batch):
+        s.import_prefix(b, synth.make_prefix_kv(cfg, ids[b], int(wl.n[b])))
+    s.set_kv_len(wl.n)
+    return s
+
+
+def planted_blocks(cfg, model, wl, seqs):
+    """Per sequence [t0, d_1..d_k]: oracle-planted drafts for `seqs`, uniform elsewhere."""
+    blocks, states = [], {}
+    for b in range(wl.batch):
+        k = int(wl.k[b])
+        if b in seqs:
+            st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+            y, _, _ = od.ar_decode(model, st, k)
+            d = synth.plant_drafts(np.array(y), int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])
+            states[b] = st
+        else:
+            d = wl.fill_any[b]
+        blocks.append(np.concatenate([[wl.t0[b]], d]).astype(np.int64))
+    return blocks, states
+
+
+def compare_sequence(cfg, sess, res, b, block, ref: od.VerifyOut, n: int, check_kv=True):
+    """Assert the parity bar for sequence b (committed length n before the step).
+
+    Returns the largest logit error seen."""
+    k = len(block) - 1
+    rows = [sess.row_of(b, i) for i in range(k + 1)]
+    err = 0.0
+    if "logits" in res:
+        err = float(np.max(np.abs(res["logits"][rows] - ref.logits)))
+        assert err <= LOGIT_TOL[cfg.dtype], f"seq {b}: logit error {err}"
+    g = res["greedy"][rows]
+    for i in range(k + 1):
+        if ref.margins[i] >= MARGIN_EXCLUDE:
+            assert g[i] == ref.greedy[i], \
+                f"seq {b} row {i}: greedy {g[i]} vs {ref.greedy[i]} (margin {ref.margins[i]})"
+    # the accept decision reads rows 0..a; compare it when none of them is excluded
+    a = ref.accepted
+    if all(ref.margins[i] >= MARGIN_EXCLUDE for i in range(a + 1)):
+        assert res["accept_len"][b] == a, f"seq {b}: accept {res['accept_len'][b]} vs {a}"
+        toks = res["out_tokens"][b]
+        assert list(toks[: a + 1]) == ref.emitted and np.all(toks[a + 1:] == -1)
+    if check_kv:
+        kv = sess.export_prefix(b, n + k + 1)
+        for layer, (kb, vb) in enumerate(ref.block_kv):
+            kv_close(kv[layer, 0, n:], kb, f"seq {b} layer {layer} K", cfg.dtype)
+            kv_close(kv[layer, 1, n:], vb, f"seq {b} layer {layer} V", cfg.dtype)
+    return err
+
+
+def kv_close(gpu: np.ndarray, want: np.ndarray, what: str, dtype: str):
+    """Cache values written by the step against the oracle's stored values.
+
+    bf16: at most one bf16 unit in the last place apart, and at least 99% bit-equal (a
+    float32 accumulation lands on the other side of a bf16 rounding boundary only when
+    it is within ~1e-6 relative of it).  float32: within 1e-5 relative + 1e-6 absolute,
+    the spread of a float32 accumulation against a float64 one.
+    """
+    want = np.asarray(want, np.float64)
+    diff = np.abs(gpu.astype(np.float64) - want)
+    if dtype == "bf16":
+        bad = diff > np.abs(want) * 2.0 ** -7 + 1e-30
+        assert not np.any(bad), f"{what}: {int(bad.sum())} cache values differ by more than one ulp"
+        exact = np.mean(diff == 0)
+        assert exact >= 0.99, f"{what}: only {exact:.4f} of cache values bit-equal"
+    else:
+        bad = diff > np.abs(want) * 1e-5 + 1e-6
+        assert not np.any(bad), f"{what}: {int(bad.sum())} cache values off by more than 1e-5"

@@ -1,0 +1,103 @@
+"""Host-only checks of libad.so: it loads, exports every entry point include/ad.h
+declares, and rejects bad arguments before touching the GPU (CPU only)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ad.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ad_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def ad():
+    from paper_2608_12703_amd import ad as mod
+    return mod
+
+
+def test_every_declared_function_is_exported(ad):
+    declared = _declared()
+    assert "ad_verify_step" in declared and "ad_kv_commit" in declared and "ad_draft_heads" in declared
+    for name in declared:
+        assert hasattr(ad.LIB, name), f"{name} declared in ad.h but not exported"
+    assert sorted(ad.EXPORTS) == declared
+
+
+def _tiny():
+    from paper_2608_12703_amd.configs import Config
+    return Config(name="t", n_layers=2, d_model=128, n_heads=2, d_ffn=256, vocab=100, dtype="bf16",
+                  batch=2, k=3)
+
+
+def test_param_count_and_model_validation(ad):
+    cfg = _tiny()
+    assert ad.param_count(cfg) == 4 + 20 * 2
+    desc = ad.model_desc(cfg)
+    h = ctypes.c_void_p()
+    fake = (ctypes.c_void_p * 44)(*([0x1000] * 44))
+    assert ad.LIB.ad_model_create(ctypes.byref(desc), fake, 43, ctypes.byref(h)) == -1
+    bad = ad.model_desc(cfg.with_(d_model=100))
+    assert ad.LIB.ad_model_create(ctypes.byref(bad), fake, 44, ctypes.byref(h)) == -5
+    assert b"64 * n_heads" in ad.LIB.ad_last_error()
+    bad = ad.model_desc(cfg.with_(vocab=0))
+    assert ad.LIB.ad_model_create(ctypes.byref(bad), fake, 44, ctypes.byref(h)) == -2
+    desc.dtype = 7
+    assert ad.LIB.ad_model_create(ctypes.byref(desc), fake, 44, ctypes.byref(h)) == -1
+    nulls = (ctypes.c_void_p * 44)(*([0x1000] * 43 + [0]))
+    assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), nulls, 44, ctypes.byref(h)) == -1
+    assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
+    n = ctypes.c_size_t()
+    assert ad.LIB.ad_workspace_size(h, 8, 2, ctypes.byref(n)) == 0 and n.value > 0
+    assert ad.LIB.ad_workspace_size(h, 0, 2, ctypes.byref(n)) == -2
+    ad.LIB.ad_model_destroy(h)
+
+
+def _step(ad, **over):
+    kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
+    cross = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
+    s = ad.Step(2, ad.AD_PADDED, 3, 8, 0x1000, 0x1000, None, kv, cross, 0x1000, 0x1000, None, None,
+                None, None, 0x1000, 0x1000, 1 << 40)
+    for k, v in over.items():
+        setattr(s, k, v)
+    return s
+
+
+def test_verify_step_rejects_before_enqueue(ad):
+    cfg = _tiny()
+    fake = (ctypes.c_void_p * 44)(*([0x1000] * 44))
+    h = ctypes.c_void_p()
+    assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
+    run = lambda s: ad.LIB.ad_verify_step(h, ctypes.byref(s), None)
+    assert run(_step(ad, tokens=None)) == -1
+    assert run(_step(ad, layout=5)) == -1
+    assert run(_step(ad, layout=ad.AD_PACKED)) == -1               # packed without cu_rows
+    assert run(_step(ad, batch=0)) == -2
+    assert run(_step(ad, k_max=448)) == -2
+    assert run(_step(ad, rows=7)) == -2                             # padded rows != B (k_max+1)
+    assert run(_step(ad, layout=ad.AD_PACKED, cu_rows=0x1000, rows=9)) == -2
+    s = _step(ad)
+    s.cross.frames_cap = 20
+    assert run(s) == -2
+    assert run(_step(ad, workspace_bytes=100)) == -3
+    assert b"workspace" in ad.LIB.ad_last_error()
+    assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1
+    assert ad.LIB.ad_kv_commit(0x1000, 0x1000, 0, None) == -2
+    kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
+    assert ad.LIB.ad_kv_import(h, ctypes.byref(kv), 0, 0x1000, 449, 0x1000, None) == -2
+    assert ad.LIB.ad_kv_export(h, ctypes.byref(kv), -1, 0x1000, 3, 0x1000, None) == -2
+    cross = ad.Cross(0x1000, 17, 0x1000, 0x1000)
+    assert ad.LIB.ad_cross_kv_prefill(h, 0x1000, ctypes.byref(cross), None) == -2
+    ws = ctypes.c_size_t()
+    assert ad.LIB.ad_draft_heads_workspace_size(h, 4, 1, ctypes.byref(ws)) == 0
+    assert ad.LIB.ad_draft_heads(h, 0x1000, 4, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
+                                 0x1000, ws.value - 1, None) == -3
+    assert ad.LIB.ad_draft_heads(h, 0x1000, 0, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
+                                 0x1000, ws.value, None) == -2
+    ad.LIB.ad_model_destroy(h)

@@ -1,0 +1,176 @@
+"""GPU parity of the verify step against the CPU oracle on small seeded shapes.
+
+Shapes span several 16-key tiles and 64-key chunks with ragged tails: draft lengths
+0..5, committed lengths 0..80, encoder lengths 1..150, vocab 1000.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from paper_2608_12703_amd import ad, synth
+from paper_2608_12703_amd.configs import Config, MAX_POS
+from paper_2608_12703_amd.harness import Session
+
+from gpu_common import (compare_sequence, device_session, oracle_model, oracle_state,
+                        planted_blocks, subset)
+
+pytestmark = pytest.mark.gpu
+
+UNIT = Config(name="unit", n_layers=2, d_model=128, n_heads=2, d_ffn=256, vocab=1000,
+              dtype="bf16", batch=5, k=5, k_min=0, frames=150, frames_min=1, kv_max=80,
+              geo_p=0.3, seed=3)
+
+
+def _setup(dtype, seed=3):
+    cfg = UNIT.with_(dtype=dtype, seed=seed)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    return cfg, params, wl
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", [ad.AD_PADDED, ad.AD_PACKED])
+def test_step_matches_oracle(dtype, layout):
+    cfg, params, wl = _setup(dtype)
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, set(range(wl.batch)))
+    sess = device_session(cfg, params, wl, layout=layout, packed_encoder=layout == ad.AD_PACKED,
+                          poison=True)
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    worst = 0.0
+    for b in range(wl.batch):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:])
+        worst = max(worst, compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b])))
+    print(f"[{dtype} layout={layout}] max logit error {worst:.3e}")
+    # planted agreement: acceptance is min(G, k) where the oracle is decisive
+    assert np.all(res["accept_len"] <= wl.k)
+    sess.commit()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sess.kv_len.cpu().numpy(), wl.n + res["accept_len"] + 1)
+
+
+def test_layouts_are_bit_identical():
+    cfg, params, wl = _setup("bf16")
+    blocks = [np.concatenate([[wl.t0[b]], wl.fill_any[b]]) for b in range(wl.batch)]
+    outs = []
+    for layout, packed_enc in [(ad.AD_PADDED, False), (ad.AD_PACKED, True), (ad.AD_PACKED, False)]:
+        sess = device_session(cfg, params, wl, layout=layout, packed_encoder=packed_enc)
+        sess.step(blocks)
+        r = sess.results()
+        hid = np.concatenate([r["hidden"][[sess.row_of(b, i) for i in range(len(blocks[b]))]]
+                              for b in range(wl.batch)])
+        outs.append((r["accept_len"], r["out_tokens"], hid))
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o[0], outs[0][0])
+        np.testing.assert_array_equal(o[1], outs[0][1])
+        np.testing.assert_array_equal(o[2].view(np.uint32), outs[0][2].view(np.uint32))
+
+
+def test_sequence_result_does_not_depend_on_batch():
+    cfg, params, wl = _setup("bf16")
+    blocks = [np.concatenate([[wl.t0[b]], wl.fill_any[b]]) for b in range(wl.batch)]
+    full = device_session(cfg, params, wl)
+    full.step(blocks)
+    rf = full.results()
+    b = 3
+    one = device_session(cfg, params, subset(wl, [b]), k_max=full.k_max, seq_ids=[b])
+    one.step(blocks[b:b + 1])
+    r1 = one.results()
+    rows = [full.row_of(b, i) for i in range(len(blocks[b]))]
+    np.testing.assert_array_equal(r1["hidden"][:len(rows)].view(np.uint32),
+                                  rf["hidden"][rows].view(np.uint32))
+    assert r1["accept_len"][0] == rf["accept_len"][b]
+
+
+def test_gpu_speculative_equals_gpu_autoregressive():
+    """Losslessness on the GPU itself: speculative rounds emit the AR tokens exactly."""
+    cfg, params, wl = _setup("bf16", seed=5)
+    B, steps = 3, 30
+    wl3 = synth.make_step_workload(cfg, batch=B)
+    sess = device_session(cfg, params, wl3, k_max=6)
+    # AR reference: one token per round
+    pend = [int(t) for t in wl3.t0]
+    ys = [[] for _ in range(B)]
+    for _ in range(steps):
+        sess.step([[p] for p in pend], commit=True)
+        r = sess.results()
+        assert r["err"] == 0
+        pend = [int(r["out_tokens"][b][0]) for b in range(B)]
+        for b in range(B):
+            ys[b].append(pend[b])
+    # speculative: drafts planted from the AR tokens with geometric agreement
+    sess.set_kv_len(wl3.n)
+    g = np.random.default_rng(11)
+    got = [[] for _ in range(B)]
+    pend = [int(t) for t in wl3.t0]
+    while min(len(x) for x in got) < steps:
+        blocks = []
+        for b in range(B):
+            pos = len(got[b])
+            k = max(0, min(6, steps - pos))
+            y = np.array(ys[b][pos: pos + k])
+            G = int(g.geometric(0.35)) - 1
+            d = synth.plant_drafts(y, G, g.integers(0, cfg.vocab - 1, k), g.integers(0, cfg.vocab, k))
+            blocks.append(np.concatenate([[pend[b]], d[:len(y)]]))
+        sess.step(blocks, commit=True)
+        r = sess.results()
+        assert r["err"] == 0
+        for b in range(B):
+            a = int(r["accept_len"][b])
+            got[b] += [int(t) for t in r["out_tokens"][b][: a + 1]]
+            pend[b] = got[b][-1]
+    for b in range(B):
+        assert got[b][:steps] == ys[b], f"sequence {b} diverged from AR"
+
+
+def test_device_detected_errors_skip_the_sequence():
+    cfg, params, wl = _setup("bf16")
+    sess = device_session(cfg, params, wl)
+    blocks = [np.concatenate([[wl.t0[b]], wl.fill_any[b]]) for b in range(wl.batch)]
+    blocks[1] = blocks[1].copy()
+    blocks[1][0] = cfg.vocab + 5                       # token outside the vocabulary
+    sess.step(blocks, commit=True)
+    r = sess.results()
+    assert r["err"] & ad.AD_ERR_TOKEN
+    assert r["accept_len"][1] == -1 and np.all(r["out_tokens"][1] == -1)
+    assert r["kv_len"][1] == wl.n[1]                   # not advanced
+    assert np.all(r["accept_len"][[0, 2, 3, 4]] >= 0)
+    # a page outside the pool
+    sess.err_flag.zero_()
+    sess.set_kv_len(wl.n)
+    page = int(sess.block_table[2, 0].item())
+    sess.block_table[2, 0] = sess.num_pages + 3
+    blocks[1][0] = wl.t0[1]
+    sess.step(blocks)
+    r = sess.results()
+    assert r["err"] & ad.AD_ERR_PAGE and r["accept_len"][2] == -1
+    # a block running past the last position
+    sess.err_flag.zero_()
+    sess.block_table[2, 0] = page
+    n = wl.n.copy()
+    n[3] = MAX_POS - len(blocks[3]) + 1
+    sess.set_kv_len(n)
+    sess.step(blocks)
+    r = sess.results()
+    assert r["err"] & ad.AD_ERR_LENGTH and r["accept_len"][3] == -1
+
+
+def test_block_ending_at_last_position():
+    cfg, params, wl = _setup("bf16")
+    model = oracle_model(cfg, params)
+    b = 0
+    k = int(wl.k[b])
+    n = MAX_POS - 1 - k
+    wl.n[b] = n
+    sess = device_session(cfg, params, wl)
+    blocks = [np.concatenate([[wl.t0[i]], wl.fill_any[i]]) for i in range(wl.batch)]
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    st = oracle_state(cfg, model, b, n, int(wl.T[b]), int(wl.t0[b]))
+    ref = od.verify(model, st, blocks[b][1:])
+    compare_sequence(cfg, sess, res, b, blocks[b], ref, n)
