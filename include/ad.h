@@ -156,9 +156,10 @@ typedef struct {
   size_t workspace_bytes;
 } ad_step;
 
-/* Bytes of workspace a step with up to max_rows rows and max_batch sequences needs. */
+/* Bytes of workspace a step with up to max_rows rows, max_batch sequences and draft
+ * length up to k_max needs. */
 ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max_batch,
-                            size_t* bytes);
+                            int32_t k_max, size_t* bytes);
 
 /*
  * Setup, once per utterance (not part of the per-round step): project encoder states

@@ -57,7 +57,7 @@ def _load():
         "ad_model_create": (_i32, [ctypes.POINTER(ModelDesc), ctypes.POINTER(_ptr), _i32,
                                    ctypes.POINTER(_ptr)]),
         "ad_model_destroy": (_i32, [_ptr]),
-        "ad_workspace_size": (_i32, [_ptr, _i32, _i32, ctypes.POINTER(_size)]),
+        "ad_workspace_size": (_i32, [_ptr, _i32, _i32, _i32, ctypes.POINTER(_size)]),
         "ad_cross_kv_prefill": (_i32, [_ptr, _ptr, ctypes.POINTER(Cross), _ptr]),
         "ad_verify_step": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
         "ad_kv_commit": (_i32, [_ptr, _ptr, _i32, _ptr]),
@@ -127,9 +127,10 @@ class Model:
               "ad_model_create")
         self.handle = h
 
-    def workspace_size(self, rows: int, batch: int) -> int:
+    def workspace_size(self, rows: int, batch: int, k_max: int) -> int:
         n = _size()
-        check(LIB.ad_workspace_size(self.handle, rows, batch, ctypes.byref(n)), "ad_workspace_size")
+        check(LIB.ad_workspace_size(self.handle, rows, batch, k_max, ctypes.byref(n)),
+              "ad_workspace_size")
         return n.value
 
     def draft_heads_workspace_size(self, n_heads: int, batch: int) -> int:

@@ -1,5 +1,6 @@
 // C-ABI entry points of libad.so: argument validation, workspace layout and the order
 // of kernel launches that makes one verify step.
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -41,18 +42,25 @@ const void* lp(const ad_model* m, int layer, int which) {
 struct Workspace {
   ad::SeqDesc* seqs;
   ad::RowDesc* rows;
-  float* x;       // residual stream [M][d]
-  float* ln;      // LayerNorm output [M][d]
-  float* q;       // queries [M][d]
-  float* att;     // attention output [M][d]
-  float* hid;     // GELU output [M][F]
-  float* hidden;  // final LayerNorm output [M][d]
-  float* logits;  // [M][V]
-  int* greedy;    // [M]
+  float* x;        // residual stream [M][d]
+  float* ln;       // float32 path: LayerNorm output [M][d]
+  float* q;        // queries [M][d]
+  float* att;      // float32 path: attention output [M][d]
+  float* hid;      // float32 path: GELU output [M][F]
+  float* hidden;   // final LayerNorm output [M][d]
+  float* logits;   // float32 path: [M][V]
+  int* greedy;     // [M]
+  uint16_t* afrag; // bf16 path: d-wide product operand, A-fragment order
+  uint16_t* hfrag; // bf16 path: F-wide product operand (GELU output)
+  float* gpart;    // bf16 path: split-K partial products
+  void* ampart;    // bf16 path: LM-head top-2 records
+  int RT, qgroups;
   size_t bytes;
 };
 
-Workspace carve(const ad_model_desc& d, int M, int B, char* base) {
+int div_up(int a, int b) { return (a + b - 1) / b; }
+
+Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
   Workspace w{};
   size_t off = 0;
   auto take = [&](size_t n) {
@@ -60,16 +68,31 @@ Workspace carve(const ad_model_desc& d, int M, int B, char* base) {
     off += align256(n);
     return p;
   };
+  const size_t D = d.d_model, F = d.d_ffn, V = d.vocab;
+  w.RT = div_up(div_up(M, 16), 16) * 16;  // row tiles of the product operands
+  w.qgroups = div_up(k_max + 1, 16);
   w.seqs = (ad::SeqDesc*)take(sizeof(ad::SeqDesc) * (size_t)B);
   w.rows = (ad::RowDesc*)take(sizeof(ad::RowDesc) * (size_t)M);
-  w.x = (float*)take(4ull * M * d.d_model);
-  w.ln = (float*)take(4ull * M * d.d_model);
-  w.q = (float*)take(4ull * M * d.d_model);
-  w.att = (float*)take(4ull * M * d.d_model);
-  w.hid = (float*)take(4ull * M * d.d_ffn);
-  w.hidden = (float*)take(4ull * M * d.d_model);
-  w.logits = (float*)take(4ull * M * d.vocab);
+  w.x = (float*)take(4 * M * D);
+  w.q = (float*)take(4 * M * D);
+  w.hidden = (float*)take(4 * M * D);
   w.greedy = (int*)take(4ull * M);
+  if (d.dtype == AD_F32) {
+    w.ln = (float*)take(4 * M * D);
+    w.att = (float*)take(4 * M * D);
+    w.hid = (float*)take(4 * M * F);
+    w.logits = (float*)take(4 * M * V);
+  } else {
+    const int Mp = w.RT * 16;
+    w.afrag = (uint16_t*)take(4ull * Mp * D);
+    w.hfrag = (uint16_t*)take(4ull * Mp * F);
+    size_t gp = 0;
+    const int shapes[6][2] = {{3 * (int)D, (int)D}, {(int)D, (int)D}, {(int)D, (int)D},
+                              {(int)D, (int)D}, {(int)F, (int)D}, {(int)D, (int)F}};
+    for (auto& sh : shapes) gp = std::max(gp, ad::gemm_part_floats(M, sh[0], sh[1]));
+    w.gpart = (float*)take(4 * gp);
+    w.ampart = take(16ull * M * ad::lm_tiles((int)V));
+  }
   w.bytes = off;
   return w;
 }
@@ -98,7 +121,7 @@ struct ProfScope {
 };
 
 template <class S>
-void run_step(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
+void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
   const ad_model_desc& D = m->desc;
   const int M = s->rows, d = D.d_model, F = D.d_ffn, H = D.n_heads, V = D.vocab;
   ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
@@ -160,6 +183,89 @@ void run_step(const ad_model* m, const ad_step* s, const Workspace& w, hipStream
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
 }
 
+// bf16 model.  Every projection writes split-K partial products; the next kernel
+// finishes them: the attention kernels (queries, and the block's keys / values into the
+// cache), the residual + LayerNorm row kernel, or the GELU reduction.
+void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
+  const ad_model_desc& D = m->desc;
+  const int M = s->rows, d = D.d_model, F = D.d_ffn, H = D.n_heads, V = D.vocab, RT = w.RT;
+  ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
+                 s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
+                 s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
+                 s->cross.frames_cap};
+  ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
+  ad::launch_embed_ln(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, lp(m, 0, LN1_G), lp(m, 0, LN1_B),
+                      w.afrag, RT, st);
+
+  auto gemm = [&](int epi, int N, int K, const uint16_t* A, const void* W, ad::EpiArgs e, int prof) {
+    ad::GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.RT = RT; g.A = A;
+    g.W = (const uint16_t*)W;
+    g.part = w.gpart;
+    g.e = e;
+    ProfScope ps(m, prof, st);
+    ad::launch_gemm_mfma(epi, g, st);
+  };
+  const ad::EpiArgs none{};
+  ad::AttnArgs at{};
+  at.H = H; at.d = d; at.seqs = w.seqs; at.out = w.afrag; at.out_RT = RT;
+  at.num_pages = s->kv.num_pages; at.block_table = s->kv.block_table;
+  at.pages_per_seq = s->kv.pages_per_seq; at.frames_cap = s->cross.frames_cap;
+  at.qgroups = w.qgroups; at.qkv_part = w.gpart; at.rows = M;
+
+  for (int l = 0; l < D.n_layers; ++l) {
+    at.layer = l;
+    // self-attention sublayer (LN1 was applied by the previous row kernel)
+    gemm(ad::EPI_PARTIAL, 3 * d, d, w.afrag, lp(m, l, W_QKV), none, AD_PROF_GEMM);
+    at.cross = 0; at.kv = (const uint16_t*)s->kv.pool; at.chunk = ad::kSelfChunk;
+    at.max_chunks = div_up(D.max_pos, ad::kSelfChunk);
+    at.qkv_splits = ad::gemm_splits(3 * d, d); at.qkv_n = 3 * d;
+    at.qkv_bias = (const uint16_t*)lp(m, l, B_QKV);
+    {
+      ProfScope ps(m, AD_PROF_SELF_ATTN, st);
+      ad::launch_attn_mfma(at, s->batch, st);
+    }
+    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_O), none, AD_PROF_GEMM);
+    ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_O), w.x,
+                             lp(m, l, LN2_G), lp(m, l, LN2_B), w.afrag, RT, nullptr, st);
+    // cross-attention sublayer
+    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XQ), none, AD_PROF_GEMM);
+    at.cross = 1; at.kv = (const uint16_t*)s->cross.data; at.chunk = ad::kCrossChunk;
+    at.max_chunks = div_up(D.max_frames, ad::kCrossChunk);
+    at.qkv_splits = ad::gemm_splits(d, d); at.qkv_n = d;
+    at.qkv_bias = (const uint16_t*)lp(m, l, B_XQ);
+    {
+      ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
+      ad::launch_attn_mfma(at, s->batch, st);
+    }
+    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XO), none, AD_PROF_GEMM);
+    ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_XO), w.x,
+                             lp(m, l, LN3_G), lp(m, l, LN3_B), w.afrag, RT, nullptr, st);
+    // feed-forward sublayer
+    gemm(ad::EPI_PARTIAL, F, d, w.afrag, lp(m, l, W_1), none, AD_PROF_GEMM);
+    {
+      ad::GemmArgs g{};
+      g.M = M; g.N = F; g.K = d; g.RT = RT; g.part = w.gpart;
+      g.bias = (const uint16_t*)lp(m, l, B_1);
+      g.e.frag = w.hfrag; g.e.frag_RT = RT;
+      ad::launch_gelu_reduce(g, st);
+    }
+    gemm(ad::EPI_PARTIAL, d, F, w.hfrag, lp(m, l, W_2), none, AD_PROF_GEMM);
+    const bool last = l + 1 == D.n_layers;
+    float* hidden = s->out_hidden ? s->out_hidden : w.hidden;
+    ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, F), w.gpart, lp(m, l, B_2), w.x,
+                             last ? m->p[P_LNF_G] : lp(m, l + 1, LN1_G),
+                             last ? m->p[P_LNF_B] : lp(m, l + 1, LN1_B), w.afrag, RT,
+                             last ? hidden : nullptr, st);
+  }
+  ad::EpiArgs e{};
+  e.out = s->out_logits; e.ldo = V; e.am_part = w.ampart;
+  gemm(ad::EPI_ARGMAX, V, d, w.afrag, m->p[P_TOK], e, AD_PROF_LM_HEAD);
+  int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
+  ad::launch_argmax_final(M, ad::lm_tiles(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
+  ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+}
+
 ad_status validate_desc(const ad_model_desc* d) {
   if (!d) return fail(AD_EINVAL, "model descriptor is NULL");
   if (d->dtype != AD_F32 && d->dtype != AD_BF16) return fail(AD_EINVAL, "unknown dtype");
@@ -169,6 +275,8 @@ ad_status validate_desc(const ad_model_desc* d) {
   if (d->d_model != AD_HEAD_DIM * d->n_heads)
     return fail(AD_EUNSUPPORTED, "d_model must equal 64 * n_heads");
   if (d->d_ffn % 64 != 0) return fail(AD_EUNSUPPORTED, "d_ffn must be a multiple of 64");
+  if (d->max_frames > 8 * ad::kCrossChunk || d->max_pos > 8 * ad::kSelfChunk)
+    return fail(AD_EUNSUPPORTED, "max_frames must be <= 2048 and max_pos <= 1024");
   return AD_OK;
 }
 
@@ -253,10 +361,12 @@ ad_status ad_profile_read(ad_model* model, double* total_ms, int32_t* launches) 
   return AD_OK;
 }
 
-ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max_batch, size_t* bytes) {
+ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max_batch,
+                            int32_t k_max, size_t* bytes) {
   if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
-  if (max_rows <= 0 || max_batch <= 0) return fail(AD_ERANGE, "max_rows and max_batch must be positive");
-  *bytes = carve(model->desc, max_rows, max_batch, nullptr).bytes;
+  if (max_rows <= 0 || max_batch <= 0 || k_max < 0)
+    return fail(AD_ERANGE, "max_rows and max_batch must be positive, k_max non-negative");
+  *bytes = carve(model->desc, max_rows, max_batch, k_max, nullptr).bytes;
   return AD_OK;
 }
 
@@ -279,14 +389,14 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->kv.num_pages < 1 || s->kv.pages_per_seq < 1) return fail(AD_ERANGE, "empty page pool");
   if (s->cross.frames_cap < ad::kTile || s->cross.frames_cap % ad::kTile)
     return fail(AD_ERANGE, "frames_cap must be a positive multiple of 16");
-  const Workspace need = carve(D, s->rows, s->batch, nullptr);
+  const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");
   (void)hipGetLastError();
-  const Workspace w = carve(D, s->rows, s->batch, (char*)s->workspace);
+  const Workspace w = carve(D, s->rows, s->batch, s->k_max, (char*)s->workspace);
   hipStream_t st = (hipStream_t)stream;
-  if (D.dtype == AD_BF16) run_step<ad::BF16>(model, s, w, st);
-  else run_step<ad::F32>(model, s, w, st);
+  if (D.dtype == AD_BF16) run_step_mfma(model, s, w, st);
+  else run_step_valu<ad::F32>(model, s, w, st);
   return check_hip("ad_verify_step");
 }
 

@@ -68,8 +68,10 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 }
 
 // ----------------------------------------------------------------- cache layouts
-// Self-KV pool: [layer][K|V][page][head][tile]; cross-KV: [layer][K|V][head][frame].
-// Inside a 16 x 64 tile element (token t, lane j) sits at t * 64 + j.
+// Self-KV pool: [layer][K|V][page][head][tile]; cross-KV: [layer][K|V][head][frame tile].
+// A 16-token x 64-lane tile holds keys token-major (t * 64 + j: a token's 64 lanes are
+// one 128-byte line) and values lane-major (j * 16 + t: the 16 tokens of one lane are
+// contiguous, the order the value operand of the P.V product is read in).
 
 __device__ __forceinline__ size_t kv_tile_base(int layer, int kv, int page, int head,
                                                int num_pages, int H) {
@@ -78,7 +80,57 @@ __device__ __forceinline__ size_t kv_tile_base(int layer, int kv, int page, int 
 __device__ __forceinline__ size_t cross_base(int layer, int kv, int head, int H, int frames_cap) {
   return (((size_t)layer * 2 + kv) * H + head) * (size_t)frames_cap * kHead;
 }
-__device__ __forceinline__ int tile_off(int t, int j) { return t * kHead + j; }
+__device__ __forceinline__ int tile_off(int kv, int t, int j) {
+  return kv == 0 ? t * kHead + j : j * kTile + t;
+}
+// element (frame f, lane j) of one head's cross K (kv = 0) or V (kv = 1)
+__device__ __forceinline__ size_t cross_off(int kv, int f, int j) {
+  return (size_t)(f / kTile) * kTileElems + tile_off(kv, f % kTile, j);
+}
+
+// ----------------------------------------------------------------- MFMA operands
+// gfx950 v_mfma_f32_16x16x32_bf16: lane l supplies 8 bf16 of row (l % 16) of A and 8 of
+// column (l % 16) of B for the same 8 reduction slots, and receives D rows
+// 4 (l / 16) .. 4 (l / 16) + 3 of column l % 16.  Lane group g = l / 16 supplies
+// reduction elements 8 g .. 8 g + 7 of each 32-wide block.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Float32 activations enter bf16 products as a pair hi = bf16(v), lo = bf16(v - hi)
+// (v - hi is exact in float32), which carries 16 significant bits into the product.
+__device__ __forceinline__ void split_hilo(float v, uint16_t& hi, uint16_t& lo) {
+  hi = f32_to_bf16(v);
+  lo = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
+// "A-fragment" order of an activation matrix X [M][K] (K a multiple of 32, RT row tiles):
+// for every 32-wide K block kb and 16-row tile rt, two 1 KB runs (hi, lo) of 64 lanes x 8
+// bf16 in the order the MFMA A operand is read; the RT tiles of one K block are
+// contiguous, so a workgroup stages a block of rows with one contiguous copy.
+__device__ __forceinline__ size_t afrag_index(int m, int k, int hilo, int RT) {
+  const int kb = k >> 5, kk = k & 31, g = kk >> 3, j = kk & 7;
+  const int rt = m >> 4, r = m & 15;
+  return (((size_t)kb * RT + rt) * 2 + hilo) * 512 + (size_t)(g * 16 + r) * 8 + j;
+}
+__device__ __forceinline__ void afrag_store(uint16_t* base, int RT, int m, int k, float v) {
+  uint16_t hi, lo;
+  split_hilo(v, hi, lo);
+  base[afrag_index(m, k, 0, RT)] = hi;
+  base[afrag_index(m, k, 1, RT)] = lo;
+}
+
+// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at lds_wave + 16 l
+// (lds_wave must be the same for the whole wave).
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
+  __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
+                                   (void __attribute__((address_space(3)))*)lds_wave, 16, 0, 0);
+}
 
 // ----------------------------------------------------------------- step descriptors
 // Built by the prep kernel from the caller's device arrays, after validation.

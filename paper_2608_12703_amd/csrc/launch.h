@@ -31,11 +31,16 @@ enum Epi : int {
   EPI_GELU = 2,    // out[m][n] = GELU(acc + bias)            (float32)
   EPI_QKV = 3,     // n < d: q; d <= n < 3d: key / value into the paged cache
   EPI_XKV = 4,     // cross-K/V prefill: n < d key, else value, into the cross cache
+  EPI_ARGMAX = 5,  // LM head: per-tile top-2 records (and optionally the logits)
+  EPI_PARTIAL = 6, // raw product (split-K partial when S > 1) into part[s][m][n]
 };
 
 struct EpiArgs {
   float* out;
   size_t ldo;
+  uint16_t* frag;   // EPI_GELU: output in A-fragment order (hi/lo) with frag_RT row tiles
+  int frag_RT;
+  void* am_part;    // EPI_ARGMAX: float4 [M][tiles] top-2 records
   // cache writes
   const RowDesc* rows;
   void* cache;
@@ -72,6 +77,66 @@ void launch_gemm_valu(int epi, int M, int N, int K, const float* A, const void* 
 // The same product with a bf16 A operand (encoder states of a bf16 model).
 void launch_gemm_valu_bf16a(int epi, int M, int N, int K, const void* A, const void* W, const void* bias,
                             const EpiArgs& e, hipStream_t st);
+
+// bf16 matrix-core product: X (A-fragment order, RT row tiles, RT a multiple of 16)
+// times W^T.
+struct GemmArgs {
+  int M, N, K, RT;
+  const uint16_t* A;
+  const uint16_t* W;
+  const uint16_t* bias;
+  int S, KB, ntiles, mchunks;  // set by the launcher
+  float* part;           // split-K partial products [S][M][N]
+  EpiArgs e;
+};
+// epi = EPI_PARTIAL (split-K partial products into `part`) or EPI_ARGMAX (LM head:
+// per-tile top-2 records into e.am_part, optional logits into e.out).
+void launch_gemm_mfma(int epi, GemmArgs g, hipStream_t st);
+// Sum the split-K partials of a preceding EPI_PARTIAL launch, add the bias, apply GELU and
+// store the result in A-fragment order (e.frag, e.frag_RT).
+void launch_gelu_reduce(GemmArgs g, hipStream_t st);
+void launch_argmax_final(int M, int ntiles, const void* part, const RowDesc* rows, int* greedy,
+                         float* margin, int* err, hipStream_t st);
+int gemm_splits(int N, int K);
+int gemm_launch_splits(int epi, int N, int K);
+size_t gemm_part_floats(int M, int N, int K);
+int lm_tiles(int V);
+
+// Matrix-core attention over bf16 caches; output in A-fragment order.
+constexpr int kAttnPart = 16 + 16 + 64 * 16;   // per chunk: max, sum, O^T (64 x 16)
+constexpr int kSelfChunk = 128;                // keys per wave, self-attention
+constexpr int kCrossChunk = 256;               // frames per wave, cross-attention
+struct AttnArgs {
+  int H, d, layer, cross;
+  const SeqDesc* seqs;
+  // the block's queries (and for self-attention its keys and values) arrive as the
+  // split-K partial products of the projection: qkv_part[s][m][n], n in [0, qkv_n)
+  const float* qkv_part;
+  int qkv_splits, qkv_n, rows;
+  const uint16_t* qkv_bias;
+  uint16_t* out;
+  int out_RT;
+  const uint16_t* kv;
+  int num_pages;
+  const int* block_table;
+  int pages_per_seq, frames_cap;
+  int chunk, max_chunks, qgroups;   // max_chunks waves per workgroup (at most 8)
+};
+void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st);
+
+// LayerNorm of float32 rows into A-fragment order (hi/lo bf16) for the next product,
+// and optionally also as float32 rows (out may be NULL).
+template <class S>
+void launch_layernorm_frag(int M, int d, const float* x, const void* g, const void* b,
+                           uint16_t* frag, int RT, float* out, hipStream_t st);
+void launch_zero_i32(int* p, int n, hipStream_t st);
+// bf16 model: x += sum of split-K partials + bias, then LayerNorm -> A fragments (and out).
+void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* bias, float* x,
+                          const void* g, const void* b, uint16_t* frag, int RT, float* out,
+                          hipStream_t st);
+// bf16 model: embedding fused with the first LayerNorm.
+void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
+                     const void* g, const void* b, uint16_t* frag, int RT, hipStream_t st);
 
 // Attention of every block row over the paged self cache (causal inside the block) or
 // over the sequence's encoder frames.  q and out are float32 [rows][d].

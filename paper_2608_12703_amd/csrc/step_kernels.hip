@@ -109,6 +109,106 @@ __global__ void __launch_bounds__(256) layernorm_kernel(int d, const float* x,
     out[(size_t)m * d + j] = (xr[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j);
 }
 
+// Same normalisation, written as the hi/lo A operand of the next bf16 product.
+template <class S>
+__global__ void __launch_bounds__(256) layernorm_frag_kernel(int d, const float* x,
+                                                             const typename S::T* g,
+                                                             const typename S::T* b,
+                                                             uint16_t* frag, int RT, float* out) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const float* xr = x + (size_t)m * d;
+  float s = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) s += xr[j];
+  const float mean = block_sum<4>(s, red) / (float)d;
+  float v = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float t = xr[j] - mean;
+    v += t * t;
+  }
+  const float var = block_sum<4>(v, red) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + 1e-5f);
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float y = (xr[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j);
+    afrag_store(frag, RT, m, j, y);
+    if (out) out[(size_t)m * d + j] = y;
+  }
+}
+
+// Split-K epilogue of the residual-writing products fused with the next LayerNorm:
+//   x[m] += sum_s P[s][m] + bias   (partials in split order)
+//   frag[m] = LN(x[m]) in A-fragment order (and, when out is given, also as float32).
+// One workgroup per row; the row is held in LDS.
+template <class S>
+__global__ void __launch_bounds__(256) reduce_res_ln_kernel(int M, int d, int nsplit,
+                                                            const float* P,
+                                                            const typename S::T* bias, float* x,
+                                                            const typename S::T* g,
+                                                            const typename S::T* b,
+                                                            uint16_t* frag, int RT, float* out) {
+  extern __shared__ float row[];
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const size_t plane = (size_t)M * d;
+  float sum = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const size_t e = (size_t)m * d + j;
+    float v = P[e];
+    for (int t = 1; t < nsplit; ++t) v += P[t * plane + e];
+    v += S::ld(bias, j);
+    const float xv = x[e] + v;
+    x[e] = xv;
+    row[j] = xv;
+    sum += xv;
+  }
+  const float mean = block_sum<4>(sum, red) / (float)d;
+  float var = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float t = row[j] - mean;
+    var += t * t;
+  }
+  const float rstd = 1.0f / sqrtf(block_sum<4>(var, red) / (float)d + 1e-5f);
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float y = (row[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j);
+    afrag_store(frag, RT, m, j, y);
+    if (out) out[(size_t)m * d + j] = y;
+  }
+}
+
+// Embedding of the block rows fused with the first LayerNorm.
+template <class S>
+__global__ void __launch_bounds__(256) embed_ln_kernel(int d, const RowDesc* rows,
+                                                       const typename S::T* tok_emb,
+                                                       const typename S::T* pos_emb, float* x,
+                                                       const typename S::T* g,
+                                                       const typename S::T* b, uint16_t* frag,
+                                                       int RT) {
+  extern __shared__ float row[];
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const RowDesc r = rows[m];
+  float sum = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float v = S::ld(tok_emb, (size_t)r.token * d + j) + S::ld(pos_emb, (size_t)r.pos * d + j);
+    x[(size_t)m * d + j] = v;
+    row[j] = v;
+    sum += v;
+  }
+  const float mean = block_sum<4>(sum, red) / (float)d;
+  float var = 0.f;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float t = row[j] - mean;
+    var += t * t;
+  }
+  const float rstd = 1.0f / sqrtf(block_sum<4>(var, red) / (float)d + 1e-5f);
+  for (int j = threadIdx.x; j < d; j += 256)
+    afrag_store(frag, RT, m, j, (row[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j));
+}
+
+__global__ void zero_i32_kernel(int* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += blockDim.x * gridDim.x) p[i] = 0;
+}
+
 // ---------------------------------------------------------------- argmax + margin
 // Per row: largest logit (lowest index on ties) and the runner-up value.
 
@@ -214,7 +314,7 @@ __global__ void kv_copy_kernel(int L, int H, int n, int b, typename S::T* lin,
     atomicOr(err, 2);
     return;
   }
-  const size_t at = kv_tile_base(layer, kv, pg, h, num_pages, H) + tile_off(p % kTile, j);
+  const size_t at = kv_tile_base(layer, kv, pg, h, num_pages, H) + tile_off(kv, p % kTile, j);
   if (EXPORT) lin[idx] = pool[at];
   else pool[at] = lin[idx];
 }
@@ -265,6 +365,34 @@ void launch_layernorm(int M, int d, const float* x, const void* g, const void* b
 }
 template void launch_layernorm<F32>(int, int, const float*, const void*, const void*, float*, hipStream_t);
 template void launch_layernorm<BF16>(int, int, const float*, const void*, const void*, float*, hipStream_t);
+
+template <class S>
+void launch_layernorm_frag(int M, int d, const float* x, const void* g, const void* b,
+                           uint16_t* frag, int RT, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(layernorm_frag_kernel<S>, dim3(M), dim3(256), 0, st, d, x,
+                     (const typename S::T*)g, (const typename S::T*)b, frag, RT, out);
+}
+template void launch_layernorm_frag<BF16>(int, int, const float*, const void*, const void*, uint16_t*, int, float*, hipStream_t);
+
+void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* bias, float* x,
+                          const void* g, const void* b, uint16_t* frag, int RT, float* out,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(reduce_res_ln_kernel<BF16>, dim3(M), dim3(256), d * sizeof(float), st, M, d,
+                     nsplit, P, (const uint16_t*)bias, x, (const uint16_t*)g, (const uint16_t*)b,
+                     frag, RT, out);
+}
+
+void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
+                     const void* g, const void* b, uint16_t* frag, int RT, hipStream_t st) {
+  hipLaunchKernelGGL(embed_ln_kernel<BF16>, dim3(M), dim3(256), d * sizeof(float), st, d, rows,
+                     (const uint16_t*)tok, (const uint16_t*)pos, x, (const uint16_t*)g,
+                     (const uint16_t*)b, frag, RT);
+}
+
+void launch_zero_i32(int* p, int n, hipStream_t st) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(zero_i32_kernel, dim3(min((n + 255) / 256, 1024)), dim3(256), 0, st, p, n);
+}
 
 void launch_argmax(int M, int V, const float* logits, size_t ld, const RowDesc* rows, int* greedy,
                    float* margin, int* err, hipStream_t st) {

@@ -64,15 +64,12 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
           int pg = e.block_table[(size_t)rd.seq * e.pages_per_seq + rd.pos / kTile];
           pg = min(max(pg, 0), e.num_pages - 1);
           S::st((typename S::T*)e.cache,
-                kv_tile_base(e.layer, kv, pg, h, e.num_pages, e.H) + tile_off(rd.pos % kTile, j), v);
+                kv_tile_base(e.layer, kv, pg, h, e.num_pages, e.H) + tile_off(kv, rd.pos % kTile, j), v);
         }
       }
     } else if (EPI == EPI_XKV) {
       const int kv = n / e.d, h = (n % e.d) / kHead, j = n % kHead;
-      S::st((typename S::T*)e.cache,
-            cross_base(e.layer, kv, h, e.H, e.frames_cap) + (size_t)(m / kTile) * kTileElems +
-                tile_off(m % kTile, j),
-            v);
+      S::st((typename S::T*)e.cache, cross_base(e.layer, kv, h, e.H, e.frames_cap) + cross_off(kv, m, j), v);
     }
   }
 }
@@ -145,14 +142,13 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
         if (t < n_keys) {
           size_t bk, bv;
           if (CROSS) {
-            const size_t off = (size_t)((s.enc_off + t) / kTile) * kTileElems + tile_off((s.enc_off + t) % kTile, j);
-            bk = cross_base(layer, 0, h, H, frames_cap) + off;
-            bv = cross_base(layer, 1, h, H, frames_cap) + off;
+            bk = cross_base(layer, 0, h, H, frames_cap) + cross_off(0, s.enc_off + t, j);
+            bv = cross_base(layer, 1, h, H, frames_cap) + cross_off(1, s.enc_off + t, j);
           } else {
             int pg = block_table[(size_t)b * pages_per_seq + t / kTile];
             pg = min(max(pg, 0), num_pages - 1);
-            bk = kv_tile_base(layer, 0, pg, h, num_pages, H) + tile_off(t % kTile, j);
-            bv = kv_tile_base(layer, 1, pg, h, num_pages, H) + tile_off(t % kTile, j);
+            bk = kv_tile_base(layer, 0, pg, h, num_pages, H) + tile_off(0, t % kTile, j);
+            bv = kv_tile_base(layer, 1, pg, h, num_pages, H) + tile_off(1, t % kTile, j);
           }
           kk = S::ld(kv, bk);
           vv = S::ld(kv, bv);

@@ -79,7 +79,7 @@ class Session:
         self.out_logits = (torch.zeros(self.max_rows, cfg.vocab, dtype=torch.float32, device=device)
                            if want_logits else None)
         self.err_flag = torch.zeros(1, **i32)
-        self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch),
+        self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch, k_max),
                                      dtype=torch.uint8, device=device)
         self.step_struct = None
 

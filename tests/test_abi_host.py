@@ -54,8 +54,9 @@ def test_param_count_and_model_validation(ad):
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), nulls, 44, ctypes.byref(h)) == -1
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
     n = ctypes.c_size_t()
-    assert ad.LIB.ad_workspace_size(h, 8, 2, ctypes.byref(n)) == 0 and n.value > 0
-    assert ad.LIB.ad_workspace_size(h, 0, 2, ctypes.byref(n)) == -2
+    assert ad.LIB.ad_workspace_size(h, 8, 2, 3, ctypes.byref(n)) == 0 and n.value > 0
+    assert ad.LIB.ad_workspace_size(h, 0, 2, 3, ctypes.byref(n)) == -2
+    assert ad.LIB.ad_workspace_size(h, 8, 2, -1, ctypes.byref(n)) == -2
     ad.LIB.ad_model_destroy(h)
 
 

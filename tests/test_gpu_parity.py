@@ -12,6 +12,7 @@ from paper_2608_12703_amd import ad, synth
 from paper_2608_12703_amd.configs import Config, MAX_POS
 from paper_2608_12703_amd.harness import Session
 
+import gpu_common
 from gpu_common import (compare_sequence, device_session, oracle_model, oracle_state,
                         planted_blocks, subset)
 
@@ -45,7 +46,9 @@ def test_step_matches_oracle(dtype, layout):
         st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
         ref = od.verify(model, st, blocks[b][1:])
         worst = max(worst, compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b])))
-    print(f"[{dtype} layout={layout}] max logit error {worst:.3e}")
+    kvx = min(gpu_common.KV_EXACT) if gpu_common.KV_EXACT else 1.0
+    gpu_common.KV_EXACT.clear()
+    print(f"[{dtype} layout={layout}] max logit error {worst:.3e}, min KV bit-equal fraction {kvx:.4f}")
     # planted agreement: acceptance is min(G, k) where the oracle is decisive
     assert np.all(res["accept_len"] <= wl.k)
     sess.commit()
