@@ -97,8 +97,10 @@ int32_t ad_model_param_count(const ad_model_desc* desc);
  * The decoder is pre-LN: x += SelfAttn(LN1 x); x += CrossAttn(LN2 x);
  * x += W2 GELU(W1 LN3 x + b1) + b2; logits = LN_f(x) tok_emb^T (the paper's
  * Whisper-large-v3 target, appendix "Whisper Cross-Architecture Check").
- * Errors: AD_EINVAL (NULL, wrong n_params, bad dtype), AD_EUNSUPPORTED
- * (d != 64 H, d or F not a multiple of 64), AD_ERANGE (non-positive sizes).
+ * Every parameter pointer must be 16-byte aligned (kernels load 16-byte vectors).
+ * Errors: AD_EINVAL (NULL, wrong n_params, bad dtype, misaligned pointer),
+ * AD_EUNSUPPORTED (d != 64 H, H > 64, F not a multiple of 64, max_frames > 2048,
+ * max_pos > 1024), AD_ERANGE (non-positive sizes).
  */
 ad_status ad_model_create(const ad_model_desc* desc, const void* const* params,
                           int32_t n_params, ad_model** out);

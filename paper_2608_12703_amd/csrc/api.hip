@@ -274,6 +274,7 @@ ad_status validate_desc(const ad_model_desc* d) {
     return fail(AD_ERANGE, "model sizes must be positive (vocab >= 2)");
   if (d->d_model != AD_HEAD_DIM * d->n_heads)
     return fail(AD_EUNSUPPORTED, "d_model must equal 64 * n_heads");
+  if (d->n_heads > 64) return fail(AD_EUNSUPPORTED, "n_heads must be <= 64 (d_model <= 4096)");
   if (d->d_ffn % 64 != 0) return fail(AD_EUNSUPPORTED, "d_ffn must be a multiple of 64");
   if (d->max_frames > 8 * ad::kCrossChunk || d->max_pos > 8 * ad::kSelfChunk)
     return fail(AD_EUNSUPPORTED, "max_frames must be <= 2048 and max_pos <= 1024");
@@ -301,6 +302,9 @@ ad_status ad_model_create(const ad_model_desc* desc, const void* const* params, 
     return fail(AD_EINVAL, "expected " + std::to_string(ad_model_param_count(desc)) + " parameters");
   for (int i = 0; i < n_params; ++i)
     if (!params[i]) return fail(AD_EINVAL, "parameter " + std::to_string(i) + " is NULL");
+  for (int i = 0; i < n_params; ++i)
+    if ((uintptr_t)params[i] % 16)
+      return fail(AD_EINVAL, "parameter " + std::to_string(i) + " is not 16-byte aligned");
   ad_model* m = new ad_model;
   m->desc = *desc;
   m->p.assign(params, params + n_params);

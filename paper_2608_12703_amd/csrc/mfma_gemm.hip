@@ -232,14 +232,33 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
 
 // FFN up-projection epilogue: sum the S partial products of each element in split
 // order, add the bias, apply GELU and store the result as the next product's A operand.
+// One thread per 4 consecutive columns; the loads of eight splits are issued before
+// their sums.
 __global__ void __launch_bounds__(256) gelu_reduce_kernel(GemmArgs g) {
-  const size_t total = (size_t)g.M * g.N;
-  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
-    float v = g.part[e];
-    for (int t = 1; t < g.S; ++t) v += g.part[(size_t)t * total + e];
-    const int m = (int)(e / g.N), n = (int)(e % g.N);
-    if (g.bias) v += bf16_to_f32(g.bias[n]);
-    afrag_store(g.e.frag, g.e.frag_RT, m, n, gelu_erf(v));
+  const int n4 = g.N / 4;
+  const size_t total4 = (size_t)g.M * n4, plane = (size_t)g.M * g.N;
+  for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < total4; q += (size_t)gridDim.x * 256) {
+    const int m = (int)(q / n4), n = (int)(q % n4) * 4;
+    const size_t e = (size_t)m * g.N + n;
+    float4 acc = *(const float4*)(g.part + e);
+    for (int t0 = 1; t0 < g.S; t0 += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = *(const float4*)(g.part + (size_t)min(t0 + u, g.S - 1) * plane + e);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (t0 + u < g.S) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
+    }
+    const uint2 bu = *(const uint2*)(g.bias + n);
+    float y[4] = {gelu_erf(acc.x + bf16_to_f32(bu.x & 0xffff)), gelu_erf(acc.y + bf16_to_f32(bu.x >> 16)),
+                  gelu_erf(acc.z + bf16_to_f32(bu.y & 0xffff)), gelu_erf(acc.w + bf16_to_f32(bu.y >> 16))};
+    uint16_t h[4], l[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) split_hilo(y[i], h[i], l[i]);
+    *(uint2*)(g.e.frag + afrag_index(m, n, 0, g.e.frag_RT)) =
+        uint2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+    *(uint2*)(g.e.frag + afrag_index(m, n, 1, g.e.frag_RT)) =
+        uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
   }
 }
 
@@ -310,8 +329,8 @@ void launch_gemm_mfma(int epi, GemmArgs g, hipStream_t st) {
 
 void launch_gelu_reduce(GemmArgs g, hipStream_t st) {
   g.S = gemm_splits(g.N, g.K);
-  const size_t total = (size_t)g.M * g.N;
-  const dim3 grid((unsigned)std::min<size_t>((total + 255) / 256, 2048)), block(256);
+  const size_t total4 = (size_t)g.M * g.N / 4;
+  const dim3 grid((unsigned)std::min<size_t>((total4 + 255) / 256, 4096)), block(256);
   hipLaunchKernelGGL(gelu_reduce_kernel, grid, block, 0, st, g);
 }
 

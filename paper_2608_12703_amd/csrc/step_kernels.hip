@@ -139,39 +139,83 @@ __global__ void __launch_bounds__(256) layernorm_frag_kernel(int d, const float*
 //   x[m] += sum_s P[s][m] + bias   (partials in split order)
 //   frag[m] = LN(x[m]) in A-fragment order (and, when out is given, also as float32).
 // One workgroup per row; the row is held in LDS.
-template <class S>
-__global__ void __launch_bounds__(256) reduce_res_ln_kernel(int M, int d, int nsplit,
-                                                            const float* P,
-                                                            const typename S::T* bias, float* x,
-                                                            const typename S::T* g,
-                                                            const typename S::T* b,
-                                                            uint16_t* frag, int RT, float* out) {
-  extern __shared__ float row[];
-  __shared__ float red[4];
-  const int m = blockIdx.x;
-  const size_t plane = (size_t)M * d;
-  float sum = 0.f;
-  for (int j = threadIdx.x; j < d; j += 256) {
-    const size_t e = (size_t)m * d + j;
-    float v = P[e];
-    for (int t = 1; t < nsplit; ++t) v += P[t * plane + e];
-    v += S::ld(bias, j);
-    const float xv = x[e] + v;
-    x[e] = xv;
-    row[j] = xv;
-    sum += xv;
+// Sum over the block's waves in wave order; every thread gets the total.
+__device__ __forceinline__ float row_block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+__device__ __forceinline__ float4 ld_bf16x4(const uint16_t* p, int j) {
+  const uint2 u = *(const uint2*)(p + j);
+  return float4{bf16_to_f32(u.x & 0xffff), bf16_to_f32(u.x >> 16), bf16_to_f32(u.y & 0xffff),
+                bf16_to_f32(u.y >> 16)};
+}
+
+// Columns j .. j + 3 (j % 4 == 0) of row m in A-fragment order: they share one 8-wide
+// run, so the hi and lo halves are one 8-byte store each.
+__device__ __forceinline__ void afrag_store4(uint16_t* base, int RT, int m, int j, float4 v) {
+  uint16_t h[4], l[4];
+  split_hilo(v.x, h[0], l[0]);
+  split_hilo(v.y, h[1], l[1]);
+  split_hilo(v.z, h[2], l[2]);
+  split_hilo(v.w, h[3], l[3]);
+  *(uint2*)(base + afrag_index(m, j, 0, RT)) =
+      uint2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+  *(uint2*)(base + afrag_index(m, j, 1, RT)) =
+      uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
+}
+
+// v[u] = sum over splits t of P[t][e], in split order; the loads of eight splits are
+// issued before their sums.
+__device__ __forceinline__ float4 split_sum4(const float* P, size_t plane, size_t e, int nsplit) {
+  float4 acc = *(const float4*)(P + e);
+  for (int t0 = 1; t0 < nsplit; t0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = *(const float4*)(P + (size_t)min(t0 + u, nsplit - 1) * plane + e);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (t0 + u < nsplit) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
   }
-  const float mean = block_sum<4>(sum, red) / (float)d;
-  float var = 0.f;
-  for (int j = threadIdx.x; j < d; j += 256) {
-    const float t = row[j] - mean;
-    var += t * t;
+  return acc;
+}
+
+// Residual update and the next LayerNorm of one row: x += sum_s P[s] + bias, then
+// LN(x) * g + b goes out in A-fragment order (and to `out` when given).  One thread per
+// 4 columns (blockDim = d / 4 rounded up to whole waves).
+__global__ void __launch_bounds__(1024) reduce_res_ln_kernel(int M, int d, int nsplit,
+                                                             const float* P, const uint16_t* bias,
+                                                             float* x, const uint16_t* g,
+                                                             const uint16_t* b, uint16_t* frag,
+                                                             int RT, float* out) {
+  __shared__ float red[16];
+  const int m = blockIdx.x, j = threadIdx.x * 4;
+  const bool on = j < d;
+  const size_t e = (size_t)m * d + (on ? j : 0);
+  float4 xv{0.f, 0.f, 0.f, 0.f};
+  if (on) {
+    const float4 v = split_sum4(P, (size_t)M * d, e, nsplit);
+    const float4 bv = ld_bf16x4(bias, j);
+    xv = *(const float4*)(x + e);
+    xv.x += v.x + bv.x; xv.y += v.y + bv.y; xv.z += v.z + bv.z; xv.w += v.w + bv.w;
+    *(float4*)(x + e) = xv;
   }
-  const float rstd = 1.0f / sqrtf(block_sum<4>(var, red) / (float)d + 1e-5f);
-  for (int j = threadIdx.x; j < d; j += 256) {
-    const float y = (row[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j);
-    afrag_store(frag, RT, m, j, y);
-    if (out) out[(size_t)m * d + j] = y;
+  const float mean = row_block_sum(on ? (xv.x + xv.y) + (xv.z + xv.w) : 0.f, red) / (float)d;
+  const float4 c{xv.x - mean, xv.y - mean, xv.z - mean, xv.w - mean};
+  const float var = row_block_sum(on ? (c.x * c.x + c.y * c.y) + (c.z * c.z + c.w * c.w) : 0.f, red);
+  const float rstd = 1.0f / sqrtf(var / (float)d + 1e-5f);
+  if (on) {
+    const float4 gv = ld_bf16x4(g, j), bv = ld_bf16x4(b, j);
+    const float4 y{c.x * rstd * gv.x + bv.x, c.y * rstd * gv.y + bv.y, c.z * rstd * gv.z + bv.z,
+                   c.w * rstd * gv.w + bv.w};
+    afrag_store4(frag, RT, m, j, y);
+    if (out) *(float4*)(out + e) = y;
   }
 }
 
@@ -377,9 +421,9 @@ template void launch_layernorm_frag<BF16>(int, int, const float*, const void*, c
 void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* bias, float* x,
                           const void* g, const void* b, uint16_t* frag, int RT, float* out,
                           hipStream_t st) {
-  hipLaunchKernelGGL(reduce_res_ln_kernel<BF16>, dim3(M), dim3(256), d * sizeof(float), st, M, d,
-                     nsplit, P, (const uint16_t*)bias, x, (const uint16_t*)g, (const uint16_t*)b,
-                     frag, RT, out);
+  const int threads = (d / 4 + kWave - 1) / kWave * kWave;
+  hipLaunchKernelGGL(reduce_res_ln_kernel, dim3(M), dim3(threads), 0, st, M, d, nsplit, P,
+                     (const uint16_t*)bias, x, (const uint16_t*)g, (const uint16_t*)b, frag, RT, out);
 }
 
 void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,

@@ -50,6 +50,11 @@ def test_param_count_and_model_validation(ad):
     assert ad.LIB.ad_model_create(ctypes.byref(bad), fake, 44, ctypes.byref(h)) == -2
     desc.dtype = 7
     assert ad.LIB.ad_model_create(ctypes.byref(desc), fake, 44, ctypes.byref(h)) == -1
+    misaligned = (ctypes.c_void_p * 44)(*([0x1000] * 43 + [0x1008]))
+    assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), misaligned, 44, ctypes.byref(h)) == -1
+    assert b"aligned" in ad.LIB.ad_last_error()
+    wide = ad.model_desc(cfg.with_(d_model=64 * 65, n_heads=65))
+    assert ad.LIB.ad_model_create(ctypes.byref(wide), fake, 44, ctypes.byref(h)) == -5
     nulls = (ctypes.c_void_p * 44)(*([0x1000] * 43 + [0]))
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), nulls, 44, ctypes.byref(h)) == -1
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
