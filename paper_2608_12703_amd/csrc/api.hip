@@ -91,7 +91,7 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
                               {(int)D, (int)D}, {(int)F, (int)D}, {(int)D, (int)F}};
     for (auto& sh : shapes) gp = std::max(gp, ad::gemm_part_floats(M, sh[0], sh[1]));
     w.gpart = (float*)take(4 * gp);
-    w.ampart = take(16ull * M * ad::lm_tiles((int)V));
+    w.ampart = take(16ull * M * ad::lm_records((int)V));
   }
   w.bytes = off;
   return w;
@@ -262,7 +262,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   e.out = s->out_logits; e.ldo = V; e.am_part = w.ampart;
   gemm(ad::EPI_ARGMAX, V, d, w.afrag, m->p[P_TOK], e, AD_PROF_LM_HEAD);
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
-  ad::launch_argmax_final(M, ad::lm_tiles(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
+  ad::launch_argmax_final(M, ad::lm_records(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
 }
 

@@ -95,12 +95,12 @@ void launch_gemm_mfma(int epi, GemmArgs g, hipStream_t st);
 // Sum the split-K partials of a preceding EPI_PARTIAL launch, add the bias, apply GELU and
 // store the result in A-fragment order (e.frag, e.frag_RT).
 void launch_gelu_reduce(GemmArgs g, hipStream_t st);
-void launch_argmax_final(int M, int ntiles, const void* part, const RowDesc* rows, int* greedy,
+void launch_argmax_final(int M, int nrec, const void* part, const RowDesc* rows, int* greedy,
                          float* margin, int* err, hipStream_t st);
 int gemm_splits(int N, int K);
 int gemm_launch_splits(int epi, int N, int K);
 size_t gemm_part_floats(int M, int N, int K);
-int lm_tiles(int V);
+int lm_records(int V);
 
 // Matrix-core attention over bf16 caches; output in A-fragment order.
 constexpr int kAttnPart = 16 + 16 + 64 * 16;   // per chunk: max, sum, O^T (64 x 16)

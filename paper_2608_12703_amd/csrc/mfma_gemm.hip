@@ -2,8 +2,8 @@
 //
 // C[m][n] = sum_k X[m][k] W[n][k] with W bf16 [N][K] and X float32 activations stored as
 // a hi/lo bf16 pair in A-fragment order.  A workgroup owns 128 output columns and up to
-// RTC 16-row tiles; each of its four waves owns a quarter of the rows across all 128
-// columns.  Operands move in 32-wide K steps through LDS rings filled by direct
+// RTC 16-row tiles; its eight waves (two per SIMD, so one wave's LDS reads overlap the
+// other's matrix instructions) each own a quarter of the rows and half of the columns.  Operands move in 32-wide K steps through LDS rings filled by direct
 // global->LDS loads: activations (L2-resident) two steps ahead, weights (streamed from
 // HBM) five steps ahead.  The waits are explicit; the loop is unrolled over the ring
 // stages so every buffer is a distinct LDS object.  Small-N products split K over several
@@ -23,6 +23,10 @@ __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
+// Running top-2 of a set of logits: largest value v1 at index i1 (lowest index among
+// equal maxima), the runner-up value v2 (equal to v1 when the maximum repeats), and
+// whether a non-finite value was seen.  The merge is associative and commutative, so any
+// reduction order gives the same record.  Branch-free (selects only).
 struct Top2s {
   float v1;
   int i1;
@@ -30,11 +34,12 @@ struct Top2s {
   int bad;
 };
 __device__ __forceinline__ Top2s t2_merge(Top2s a, Top2s b) {
-  const bool a_wins = (a.v1 > b.v1) || (a.v1 == b.v1 && a.i1 < b.i1);
+  const bool aw = (a.v1 > b.v1) | ((a.v1 == b.v1) & (a.i1 < b.i1));
   Top2s r;
+  r.v1 = aw ? a.v1 : b.v1;
+  r.i1 = aw ? a.i1 : b.i1;
+  r.v2 = fmaxf(aw ? a.v2 : b.v2, aw ? b.v1 : a.v1);
   r.bad = a.bad | b.bad;
-  if (a_wins) { r.v1 = a.v1; r.i1 = a.i1; r.v2 = fmaxf(a.v2, b.v1); }
-  else        { r.v1 = b.v1; r.i1 = b.i1; r.v2 = fmaxf(b.v2, a.v1); }
   return r;
 }
 __device__ __forceinline__ Top2s t2_shfl(Top2s t, int mask) {
@@ -44,6 +49,28 @@ __device__ __forceinline__ Top2s t2_shfl(Top2s t, int mask) {
   u.v2 = __shfl_xor(t.v2, mask, kWave);
   u.bad = __shfl_xor(t.bad, mask, kWave);
   return u;
+}
+// Rotate by N lanes inside each row of 16 lanes (DPP row_ror, no LDS round trip).
+template <int N>
+__device__ __forceinline__ int ror16(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + N, 0xf, 0xf, false);
+}
+template <int N>
+__device__ __forceinline__ Top2s t2_ror16(Top2s t) {
+  Top2s u;
+  u.v1 = __int_as_float(ror16<N>(__float_as_int(t.v1)));
+  u.i1 = ror16<N>(t.i1);
+  u.v2 = __int_as_float(ror16<N>(__float_as_int(t.v2)));
+  u.bad = ror16<N>(t.bad);
+  return u;
+}
+// Merge over the 16 lanes of a row: afterwards every lane holds the row's record.
+__device__ __forceinline__ Top2s t2_row16(Top2s t) {
+  t = t2_merge(t, t2_ror16<8>(t));
+  t = t2_merge(t, t2_ror16<4>(t));
+  t = t2_merge(t, t2_ror16<2>(t));
+  t = t2_merge(t, t2_ror16<1>(t));
+  return t;
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding (they
@@ -55,20 +82,21 @@ __device__ __forceinline__ Top2s t2_shfl(Top2s t, int mask) {
     asm volatile("" ::: "memory");             \
   } while (0)
 
+// One 32-wide K step of a wave: RW row tiles (row group rg) x 4 column tiles (half ch).
 template <int RTC>
-__device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][8], const uint4* abuf,
-                                         const uint4* wbuf, int w, int lane) {
+__device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][4], const uint4* abuf,
+                                         const uint4* wbuf, int rg, int ch, int lane) {
   constexpr int RW = RTC / 4;
-  bf16x8 b[8];
+  bf16x8 b[4];
 #pragma unroll
-  for (int ct = 0; ct < 8; ++ct) b[ct] = as_bf16x8(wbuf[ct * 64 + lane]);
+  for (int ct = 0; ct < 4; ++ct) b[ct] = as_bf16x8(wbuf[(ch * 4 + ct) * 64 + lane]);
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
-    const int rt = w * RW + r;
+    const int rt = rg * RW + r;
     const bf16x8 ah = as_bf16x8(abuf[(rt * 2 + 0) * 64 + lane]);
     const bf16x8 al = as_bf16x8(abuf[(rt * 2 + 1) * 64 + lane]);
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) {
+    for (int ct = 0; ct < 4; ++ct) {
       acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
       acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
     }
@@ -76,15 +104,16 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][8], const uint4* 
 }
 
 template <int EPI, int RTC>
-__global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
+__global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   constexpr int RW = RTC / 4;            // row tiles per wave
-  constexpr int NA = RTC / 2;            // direct loads per wave for one activation stage
+  constexpr int NA = RTC / 4;            // direct loads per wave for one activation stage
   // Activation ring: 3 stages (requested 2 steps ahead); weight ring: 6 stages (requested
   // 5 steps ahead, covering HBM latency).  Distinct LDS objects, so the compiler can tell
   // a read of one stage from the direct loads still filling another.
   __shared__ uint4 sa0[RTC * 128], sa1[RTC * 128], sa2[RTC * 128];
   __shared__ uint4 sw0[512], sw1[512], sw2[512], sw3[512], sw4[512], sw5[512];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int rg = w & 3, ch = w >> 2;     // row group, column half
   const int c16 = lane & 15, grp = lane >> 4;
 
   // (split, column tile, row chunk) of this workgroup.  Workgroups are dealt
@@ -99,34 +128,30 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
   const int rt0 = mc * RTC, n0 = nt * kNT;
   const int kb0 = (s * g.KB) / g.S, kb1 = ((s + 1) * g.KB) / g.S;
 
-  f32x4 acc[RW][8];
+  f32x4 acc[RW][4];
 #pragma unroll
   for (int r = 0; r < RW; ++r)
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ct = 0; ct < 4; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = kb1 - kb0, kl = kb1 - 1;
   auto ia = [&](uint4* buf, int kb) {   // activation stage of step kb (clamped)
     const uint4* src = (const uint4*)g.A + ((size_t)min(kb, kl) * g.RT + rt0) * 128;
 #pragma unroll
     for (int ii = 0; ii < NA; ++ii) {
-      const int i = ii * 4 + w;
+      const int i = ii * 8 + w;
       dma16(src + i * 64 + lane, buf + i * 64);
     }
   };
   auto iw = [&](uint4* buf, int kb) {   // weight stage of step kb (clamped)
     const int k = min(kb, kl);
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int ct = w * 2 + t;
-      const int n = min(n0 + ct * 16 + (lane & 15), g.N - 1);
-      dma16(g.W + (size_t)n * g.K + k * 32 + (lane >> 4) * 8, buf + ct * 64);
-    }
+    const int n = min(n0 + w * 16 + (lane & 15), g.N - 1);   // column tile w
+    dma16(g.W + (size_t)n * g.K + k * 32 + (lane >> 4) * 8, buf + w * 64);
   };
   // Step j requests activations j + 2 and weights j + 5, in that order; the prologue
   // plays virtual steps -5 .. -1 so the outstanding-load count is the same everywhere:
   // at the end of step j the loads issued after A(j+1) are W(j+4), A(j+2), W(j+5).
-  constexpr int kWaitAfter = NA + 4;
+  constexpr int kWaitAfter = NA + 2;
   iw(sw0, kb0);
   iw(sw1, kb0 + 1);
   iw(sw2, kb0 + 2);
@@ -136,13 +161,13 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
   iw(sw4, kb0 + 4);
   BARRIER_VMCNT(kWaitAfter);
   int kb = kb0;
-#define GEMM_STEP(CA, CW, NXA, NXW)        \
-  {                                        \
-    ia(NXA, kb + 2);                       \
-    iw(NXW, kb + 5);                       \
-    mma_step<RTC>(acc, CA, CW, w, lane);   \
-    BARRIER_VMCNT(kWaitAfter);             \
-    ++kb;                                  \
+#define GEMM_STEP(CA, CW, NXA, NXW)            \
+  {                                            \
+    ia(NXA, kb + 2);                           \
+    iw(NXW, kb + 5);                           \
+    mma_step<RTC>(acc, CA, CW, rg, ch, lane);  \
+    BARRIER_VMCNT(kWaitAfter);                 \
+    ++kb;                                      \
   }
   for (int it = 0; it < nk / 6; ++it) {
     GEMM_STEP(sa0, sw0, sa2, sw5)
@@ -162,16 +187,16 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
   BARRIER_VMCNT(0);
 
   // row / column of accumulator element (r, ct, i) of this lane
-  const int row_base = (rt0 + w * RW) * 16 + grp * 4;   // + r * 16 + i
-  const int col_base = n0 + c16;                        // + ct * 16
+  const int row_base = (rt0 + rg * RW) * 16 + grp * 4;   // + r * 16 + i
+  const int col_base = n0 + ch * 64 + c16;               // + ct * 16
 
   // This kernel's LDS is also written by direct loads, so the compiler orders every LDS
   // access after outstanding global stores; epilogues therefore finish all their
   // cross-lane (LDS) work before the first store.
   if (EPI == EPI_ARGMAX) {
-    // LM head: top-2 of this tile's 128 columns per row.  A row's columns sit in 16
-    // lanes x 8 registers; registers are merged in column order, then the 16 lanes, so
-    // ties keep the lower index.
+    // LM head: top-2 of this wave's 64 columns per row (one record per half tile).  A
+    // row's columns sit in 16 lanes x 4 registers; the merge keeps the lowest index
+    // among equal maxima whatever the order.
     Top2s t[RW][4];
 #pragma unroll
     for (int r = 0; r < RW; ++r)
@@ -179,15 +204,16 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
       for (int i = 0; i < 4; ++i) {
         t[r][i] = Top2s{-INFINITY, 0x7fffffff, -INFINITY, 0};
 #pragma unroll
-        for (int ct = 0; ct < 8; ++ct) {
+        for (int ct = 0; ct < 4; ++ct) {
           const int n = col_base + ct * 16;
           const float v = acc[r][ct][i];
-          Top2s u{v, n, -INFINITY, 0};
-          if (!isfinite(v)) { u.v1 = -INFINITY; u.bad = 1; }
-          if (n < g.N) t[r][i] = t2_merge(t[r][i], u);
+          const bool fin = isfinite(v), in = n < g.N;
+          // columns past V are neutral; a non-finite logit flags the row
+          const Top2s u{(in & fin) ? v : -INFINITY, in ? n : 0x7fffffff, -INFINITY,
+                        (in & !fin) ? 1 : 0};
+          t[r][i] = t2_merge(t[r][i], u);
         }
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) t[r][i] = t2_merge(t[r][i], t2_shfl(t[r][i], o));
+        t[r][i] = t2_row16(t[r][i]);
       }
 #pragma unroll
     for (int r = 0; r < RW; ++r)
@@ -196,14 +222,14 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
         const int m = row_base + r * 16 + i;
         if (c16 == 0 && m < g.M) {
           float4 rec{t[r][i].v1, __int_as_float(t[r][i].i1), t[r][i].v2, __int_as_float(t[r][i].bad)};
-          ((float4*)g.e.am_part)[(size_t)m * g.ntiles + nt] = rec;
+          ((float4*)g.e.am_part)[(size_t)m * (2 * g.ntiles) + nt * 2 + ch] = rec;
         }
       }
     if (g.e.out) {
 #pragma unroll
       for (int r = 0; r < RW; ++r)
 #pragma unroll
-        for (int ct = 0; ct < 8; ++ct)
+        for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int m = row_base + r * 16 + i, n = col_base + ct * 16;
@@ -223,7 +249,7 @@ __global__ void __launch_bounds__(256) gemm_mfma_kernel(GemmArgs g) {
       const int m = row_base + r * 16 + i;
       if (m >= g.M) continue;
 #pragma unroll
-      for (int ct = 0; ct < 8; ++ct) {
+      for (int ct = 0; ct < 4; ++ct) {
         const int n = col_base + ct * 16;
         if (n < g.N) P[(size_t)m * g.N + n] = acc[r][ct][i];
       }
@@ -264,13 +290,13 @@ __global__ void __launch_bounds__(256) gelu_reduce_kernel(GemmArgs g) {
 
 // Row-wise merge of the per-tile top-2 records of the LM head: greedy token (lowest
 // index among equal maxima) and the top-1 minus top-2 margin.
-__global__ void __launch_bounds__(64) argmax_final_kernel(int M, int ntiles, const float4* part,
+__global__ void __launch_bounds__(64) argmax_final_kernel(int M, int nrec, const float4* part,
                                                           const RowDesc* rows, int* greedy,
                                                           float* margin, int* err) {
   const int m = blockIdx.x, lane = threadIdx.x;
   Top2s t{-INFINITY, 0x7fffffff, -INFINITY, 0};
-  for (int j = lane; j < ntiles; j += 64) {
-    const float4 p = part[(size_t)m * ntiles + j];
+  for (int j = lane; j < nrec; j += 64) {
+    const float4 p = part[(size_t)m * nrec + j];
     t = t2_merge(t, Top2s{p.x, __float_as_int(p.y), p.z, __float_as_int(p.w)});
   }
 #pragma unroll
@@ -283,35 +309,50 @@ __global__ void __launch_bounds__(64) argmax_final_kernel(int M, int ntiles, con
   }
 }
 
-// Row tiles per workgroup for an M-row product (the activation buffer holds a multiple
-// of 16 row tiles, so every staged block lies inside it).
-int gemm_rtc(int M) {
-  const int rt = (M + 15) / 16;
-  return rt <= 4 ? 4 : (rt <= 8 ? 8 : 16);
-}
+// Launch planning.  A workgroup's time is dominated by fixed costs (first-load latency,
+// the partial stores) plus its K steps, and a second round of workgroups costs a whole
+// extra pass, so plans keep the grid within one workgroup per CU.  Measured per-step
+// times for 4 / 8 / 16 row tiles: about 0.27 / 0.43 / 0.8 us.
+constexpr int kMaxWGs = 256;
+constexpr int kRefRows = 224;   // reference block for the split choice (32 sequences x 7 rows)
 
+static double step_us(int rtc) { return rtc == 4 ? 0.27 : (rtc == 8 ? 0.43 : 0.8); }
+static int mchunks_of(int M, int rtc) { return ((M + 15) / 16 + rtc - 1) / rtc; }
+
+// Split count of an N x K weight.  It depends on the weight shape only (never on the
+// number of rows), so every row's sums run in the same order whatever the batch.
 int gemm_splits(int N, int K) {
   const int ntiles = (N + kNT - 1) / kNT, KB = K / 32;
-  int s = 240 / ntiles;
-  s = min(s, KB);
-  s = min(s, max(1, K / 256));
-  return max(1, s);
+  double best = 1e30;
+  int best_s = 1;
+  for (int S = 1; S <= std::min(KB, 64); ++S)
+    for (int rtc : {4, 8, 16}) {
+      if (ntiles * mchunks_of(kRefRows, rtc) * S > kMaxWGs && S > 1) continue;
+      const double partial_us = (double)S * kRefRows * N * 4 / 4e6;   // ~4 TB/s
+      const double c = ((KB + S - 1) / S) * step_us(rtc) + partial_us;
+      if (c < best - 1e-9) { best = c; best_s = S; }
+    }
+  return best_s;
 }
 
-static int gemm_mchunks(int M) {
-  const int rtc = gemm_rtc(M);
-  return ((M + 15) / 16 + rtc - 1) / rtc;
+// Row tiles per workgroup: the smallest tile whose grid fits in one round (the
+// activation buffer holds a multiple of 16 row tiles, so every staged block lies in it).
+int gemm_rtc(int M, int N, int S) {
+  const int ntiles = (N + kNT - 1) / kNT;
+  for (int rtc : {4, 8})
+    if (ntiles * mchunks_of(M, rtc) * S <= kMaxWGs) return rtc;
+  return 16;
 }
 
 size_t gemm_part_floats(int M, int N, int K) { return (size_t)gemm_splits(N, K) * M * N; }
 
-int lm_tiles(int V) { return (V + kNT - 1) / kNT; }
+int lm_records(int V) { return 2 * ((V + kNT - 1) / kNT); }
 
 template <int EPI>
 static void launch_one(GemmArgs g, hipStream_t st) {
-  const int rtc = gemm_rtc(g.M);
-  g.mchunks = gemm_mchunks(g.M);
-  const dim3 grid(g.ntiles * g.S * g.mchunks), block(256);
+  const int rtc = gemm_rtc(g.M, g.N, g.S);
+  g.mchunks = mchunks_of(g.M, rtc);
+  const dim3 grid(g.ntiles * g.S * g.mchunks), block(512);
   if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4>), grid, block, 0, st, g);
   else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8>), grid, block, 0, st, g);
   else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16>), grid, block, 0, st, g);
@@ -334,9 +375,9 @@ void launch_gelu_reduce(GemmArgs g, hipStream_t st) {
   hipLaunchKernelGGL(gelu_reduce_kernel, grid, block, 0, st, g);
 }
 
-void launch_argmax_final(int M, int ntiles, const void* part, const RowDesc* rows, int* greedy,
+void launch_argmax_final(int M, int nrec, const void* part, const RowDesc* rows, int* greedy,
                          float* margin, int* err, hipStream_t st) {
-  hipLaunchKernelGGL(argmax_final_kernel, dim3(M), dim3(64), 0, st, M, ntiles, (const float4*)part,
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(M), dim3(64), 0, st, M, nrec, (const float4*)part,
                      rows, greedy, margin, err);
 }
 
