@@ -276,7 +276,9 @@ ad_status validate_desc(const ad_model_desc* d) {
     return fail(AD_EUNSUPPORTED, "d_model must equal 64 * n_heads");
   if (d->n_heads > 64) return fail(AD_EUNSUPPORTED, "n_heads must be <= 64 (d_model <= 4096)");
   if (d->d_ffn % 64 != 0) return fail(AD_EUNSUPPORTED, "d_ffn must be a multiple of 64");
-  if (d->max_frames > 8 * ad::kCrossChunk || d->max_pos > 8 * ad::kSelfChunk)
+  // one attention wave per key chunk, at most 8 waves per workgroup
+  static_assert(8 * ad::kCrossChunk >= 2048 && 8 * ad::kSelfChunk >= 1024, "chunk limits");
+  if (d->max_frames > 2048 || d->max_pos > 1024)
     return fail(AD_EUNSUPPORTED, "max_frames must be <= 2048 and max_pos <= 1024");
   return AD_OK;
 }

@@ -105,7 +105,7 @@ int lm_records(int V);
 // Matrix-core attention over bf16 caches; output in A-fragment order.
 constexpr int kAttnPart = 16 + 16 + 64 * 16;   // per chunk: max, sum, O^T (64 x 16)
 constexpr int kSelfChunk = 128;                // keys per wave, self-attention
-constexpr int kCrossChunk = 256;               // frames per wave, cross-attention
+constexpr int kCrossChunk = 384;               // frames per wave, cross-attention
 struct AttnArgs {
   int H, d, layer, cross;
   const SeqDesc* seqs;

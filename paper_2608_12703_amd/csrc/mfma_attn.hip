@@ -25,78 +25,86 @@ __device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) {
   return (uint32_t)a | ((uint32_t)b << 16);
 }
 
-// eight float32 values -> (hi, lo) bf16x8 operands
+// eight float32 values -> (hi, lo) bf16x8 operands (paired hardware conversions)
 __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
-  uint16_t h[8], l[8];
+  uint32_t h[4], l[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) split_hilo(v[j], h[j], l[j]);
-  hi = as_bf16x8(make_uint4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7])));
-  lo = as_bf16x8(make_uint4(pack2(l[0], l[1]), pack2(l[2], l[3]), pack2(l[4], l[5]), pack2(l[6], l[7])));
+  for (int j = 0; j < 4; ++j) {
+    h[j] = f32x2_to_bf16x2(v[2 * j], v[2 * j + 1]);
+    l[j] = f32x2_to_bf16x2(v[2 * j] - bf16_to_f32(h[j] & 0xffff), v[2 * j + 1] - bf16_to_f32(h[j] >> 16));
+  }
+  hi = as_bf16x8(make_uint4(h[0], h[1], h[2], h[3]));
+  lo = as_bf16x8(make_uint4(l[0], l[1], l[2], l[3]));
 }
 
-// keep the first n_keep (clamped to 0..4) bf16 elements of an 8-byte value, zero the rest
-// (selects, no branches: loads stay in flight)
-__device__ __forceinline__ uint2 mask4(uint2 v, int n_keep) {
-  const uint32_t m0 = (n_keep >= 1 ? 0x0000ffffu : 0u) | (n_keep >= 2 ? 0xffff0000u : 0u);
-  const uint32_t m1 = (n_keep >= 3 ? 0x0000ffffu : 0u) | (n_keep >= 4 ? 0xffff0000u : 0u);
-  return make_uint2(v.x & m0, v.y & m1);
+// keep the first n_keep (clamped to 0..8) bf16 elements of a 16-byte value, zero the
+// rest (selects, no branches: loads stay in flight)
+__device__ __forceinline__ uint4 mask8(uint4 v, int n_keep) {
+  auto m = [&](int lo) -> uint32_t {
+    return (n_keep > lo ? 0x0000ffffu : 0u) | (n_keep > lo + 1 ? 0xffff0000u : 0u);
+  };
+  return make_uint4(v.x & m(0), v.y & m(2), v.z & m(4), v.w & m(6));
 }
 
-// One 32-key block in registers: for each 16-key tile its two key halves (this lane's 16
-// lanes of key row c16), and for each 16-lane value tile dt the operand
-// (tile-0 tokens 4 grp .. +3 | tile-1 tokens 4 grp .. +3) of value lane 16 dt + c16.
+// One 32-key block in registers.  Key rows of the score products are interleaved: in
+// product tt, MFMA row r holds key 8 (r / 4) + 4 tt + r % 4, so after both products
+// the lanes of group g hold the scores of keys 8 g .. 8 g + 7, which is exactly the key
+// range the same lanes supply to the value product.  kt0 / kt1: this lane's key row of
+// product tt (two 16-byte halves each); v[dt]: keys 8 g .. 8 g + 7 of value lane
+// 16 dt + c16 (one 16-byte load from a lane-major tile).
 struct KVTiles {
   uint4 k00, k01, k10, k11;
   uint4 v0, v1, v2, v3;
 };
 
-// Load the two 16-key tiles of the 32-key block starting at blk.  Tiles past k_end are
-// replaced by the chunk's first tile (always valid) and their values zeroed, so every
-// lane issues the same unconditional loads.
-template <bool CROSS>
-__device__ __forceinline__ void load_tile(const AttnArgs& a, const SeqDesc& s, int h, int t0,
-                                          int k_beg, int k_end, int pg_lane, int c16, int grp,
-                                          uint4& k0, uint4& k1, uint2 (&v)[4]) {
-  const int keep = k_end - (t0 + grp * 4);
-  t0 = t0 < k_end ? t0 : k_beg;
-  const uint16_t* kb;
-  const uint16_t* vb;
-  if (CROSS) {
-    const size_t tile = (size_t)((s.enc_off + t0) / kTile) * kTileElems;
-    kb = a.kv + cross_base(a.layer, 0, h, a.H, a.frames_cap) + tile;
-    vb = a.kv + cross_base(a.layer, 1, h, a.H, a.frames_cap) + tile;
-  } else {
-    const int pg = __shfl(pg_lane, (t0 - k_beg) / kTile, kWave);
-    kb = a.kv + kv_tile_base(a.layer, 0, pg, h, a.num_pages, a.H);
-    vb = a.kv + kv_tile_base(a.layer, 1, pg, h, a.num_pages, a.H);
-  }
-  const uint16_t* kp = kb + c16 * kHead + grp * 16;
-  k0 = *(const uint4*)kp;
-  k1 = *(const uint4*)(kp + 8);
-  const uint16_t* vp = vb + grp * 4;
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) v[dt] = mask4(*(const uint2*)(vp + (dt * 16 + c16) * kTile), keep);
-}
-
-// Load the two 16-key tiles of the 32-key block starting at blk.  Tiles past k_end are
-// replaced by the chunk's first tile (always valid) and their values zeroed, so every
-// lane issues the same unconditional loads.
+// Load the 32-key block starting at blk (a multiple of 32 from the chunk start).  A
+// 16-key tile past k_end is replaced by the chunk's last tile (valid, and just read, so
+// the reload hits the cache), so every lane issues the same unconditional loads.
 template <bool CROSS>
 __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, int h, int blk,
                                            int k_beg, int k_end, int pg_lane, int c16, int grp,
                                            KVTiles& t) {
-  uint2 va[4], vb[4];
-  load_tile<CROSS>(a, s, h, blk, k_beg, k_end, pg_lane, c16, grp, t.k00, t.k01, va);
-  load_tile<CROSS>(a, s, h, blk + 16, k_beg, k_end, pg_lane, c16, grp, t.k10, t.k11, vb);
-  t.v0 = make_uint4(va[0].x, va[0].y, vb[0].x, vb[0].y);
-  t.v1 = make_uint4(va[1].x, va[1].y, vb[1].x, vb[1].y);
-  t.v2 = make_uint4(va[2].x, va[2].y, vb[2].x, vb[2].y);
-  t.v3 = make_uint4(va[3].x, va[3].y, vb[3].x, vb[3].y);
+  const uint16_t* kb[2];
+  const uint16_t* vb[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    int t0 = blk + 16 * u;
+    t0 = t0 < k_end ? t0 : k_beg + (k_end - 1 - k_beg) / kTile * kTile;
+    if (CROSS) {
+      const size_t tile = (size_t)((s.enc_off + t0) / kTile) * kTileElems;
+      kb[u] = a.kv + cross_base(a.layer, 0, h, a.H, a.frames_cap) + tile;
+      vb[u] = a.kv + cross_base(a.layer, 1, h, a.H, a.frames_cap) + tile;
+    } else {
+      const int pg = __shfl(pg_lane, (t0 - k_beg) / kTile, kWave);
+      kb[u] = a.kv + kv_tile_base(a.layer, 0, pg, h, a.num_pages, a.H);
+      vb[u] = a.kv + kv_tile_base(a.layer, 1, pg, h, a.num_pages, a.H);
+    }
+  }
+  // key rows: lane c16 of product tt reads key 8 (c16 / 4) + 4 tt + c16 % 4, i.e. tile
+  // c16 / 8, token 8 ((c16 / 4) % 2) + 4 tt + c16 % 4; lane group grp reads dims
+  // 16 grp .. 16 grp + 15 of it (the queries use the same dim order)
+  const uint16_t* kt = (c16 < 8 ? kb[0] : kb[1]) + (((c16 >> 2) & 1) * 8 + (c16 & 3)) * kHead + grp * 16;
+  t.k00 = *(const uint4*)kt;
+  t.k01 = *(const uint4*)(kt + 8);
+  t.k10 = *(const uint4*)(kt + 4 * kHead);
+  t.k11 = *(const uint4*)(kt + 4 * kHead + 8);
+  // values: keys 8 grp .. 8 grp + 7 = tile grp / 2, tokens 8 (grp % 2) .. + 7 (slots past
+  // the sequence are zeroed where the block is used)
+  const uint16_t* vt = (grp < 2 ? vb[0] : vb[1]) + (grp & 1) * 8 + c16 * kTile;
+  t.v0 = *(const uint4*)(vt + 0 * 16 * kTile);
+  t.v1 = *(const uint4*)(vt + 1 * 16 * kTile);
+  t.v2 = *(const uint4*)(vt + 2 * 16 * kTile);
+  t.v3 = *(const uint4*)(vt + 3 * 16 * kTile);
 }
 
-// One 32-key block of the online softmax and the two products.
+// One 32-key block of the online softmax and the two products.  MASKED: the block
+// reaches past k_end or past some query's causal limit; keys a query must not see get
+// probability 0 and value slots past k_end are zeroed (stale or poisoned cache slots
+// never reach the output).  Unmasked blocks skip all of that.  Queries past the group
+// (zero rows) are computed but never stored.
+template <bool MASKED>
 __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_end, int vis,
-                                             bool qvalid, int grp, const bf16x8 (&qh)[2],
+                                             int grp, const bf16x8 (&qh)[2],
                                              const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
                                              float& l_run) {
   float sv[8];
@@ -110,33 +118,34 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
     st = mfma_bf16(k1, ql[1], st);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = blk + tt * 16 + grp * 4 + i;
-      sv[tt * 4 + i] = (qvalid && key < k_end && key < vis) ? st[i] : -INFINITY;
+      const int key = blk + grp * 8 + tt * 4 + i;
+      sv[tt * 4 + i] = (!MASKED || (key < k_end && key < vis)) ? st[i] : -INFINITY;
     }
   }
-  float bm = sv[0];
-#pragma unroll
-  for (int j = 1; j < 8; ++j) bm = fmaxf(bm, sv[j]);
-  bm = fmaxf(bm, __shfl_xor(bm, 16, kWave));
-  bm = fmaxf(bm, __shfl_xor(bm, 32, kWave));
+  const float bm = rows4_max(fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                                   fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7]))));
   const float m_new = fmaxf(m_run, bm);
-  const float scale = (m_new == -INFINITY) ? 1.f : __expf(m_run - m_new);
+  // m_run = -inf (first block) gives scale 0; only a fully masked history can leave
+  // m_new = -inf, and then nothing changes
+  const float scale = (MASKED && m_new == -INFINITY) ? 1.f : __expf(m_run - m_new);
   float p[8], ps = 0.f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    p[j] = (sv[j] == -INFINITY) ? 0.f : __expf(sv[j] - m_new);
+    p[j] = (MASKED && sv[j] == -INFINITY) ? 0.f : __expf(sv[j] - m_new);
     ps += p[j];
   }
-  ps += __shfl_xor(ps, 16, kWave);
-  ps += __shfl_xor(ps, 32, kWave);
+  ps = rows4_sum(ps);
   l_run = l_run * scale + ps;
   m_run = m_new;
   bf16x8 ph, pl;
   split8(p, ph, pl);
+  const int keep = k_end - (blk + 8 * grp);
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) {
     o[dt] *= scale;
-    const bf16x8 vt = as_bf16x8(dt == 0 ? cur.v0 : (dt == 1 ? cur.v1 : (dt == 2 ? cur.v2 : cur.v3)));
+    uint4 vr = dt == 0 ? cur.v0 : (dt == 1 ? cur.v1 : (dt == 2 ? cur.v2 : cur.v3));
+    if (MASKED) vr = mask8(vr, keep);
+    const bf16x8 vt = as_bf16x8(vr);
     o[dt] = mfma_bf16(vt, ph, o[dt]);
     o[dt] = mfma_bf16(vt, pl, o[dt]);
   }
@@ -150,7 +159,7 @@ __device__ __forceinline__ float finish_proj(const AttnArgs& a, int m, int col) 
 }
 
 template <bool CROSS>
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2)))
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(3)))
 attn_mfma_kernel(AttnArgs a) {
   extern __shared__ float part[];  // [waves][kAttnPart], then the queries [16][64]
   const int h = blockIdx.x;
@@ -164,7 +173,6 @@ attn_mfma_kernel(AttnArgs a) {
   const int n_chunks = (n_keys + a.chunk - 1) / a.chunk;
   const int ch = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63, c16 = lane & 15, grp = lane >> 4;
-  const bool qvalid = c16 < nq;
   float* Pc = part + ch * kAttnPart;
   float* qs = part + a.max_chunks * kAttnPart;
 
@@ -216,13 +224,21 @@ attn_mfma_kernel(AttnArgs a) {
 
     // ping-pong over 32-key blocks; a block past the chunk end is fully masked and
     // leaves the state bit-for-bit unchanged
-    KVTiles ta, tb;
-    load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
-    for (int blk = k_beg; blk < k_end; blk += 64) {
-      load_block<CROSS>(a, s, h, blk + 32, k_beg, k_end, pg_lane, c16, grp, tb);
-      attend_block(ta, blk, k_end, vis, qvalid, grp, qh, ql, o, m_run, l_run);
-      load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
-      attend_block(tb, blk + 32, k_end, vis, qvalid, grp, qh, ql, o, m_run, l_run);
+    {
+      KVTiles ta, tb;
+      load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
+      // blocks below `clean` need no masking for any query of the group
+      const int clean = CROSS ? k_end : min(k_end, s.n + q0 + 1);
+      auto attend = [&](const KVTiles& t, int blk) {
+        if (blk + 32 <= clean) attend_block<false>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+        else attend_block<true>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+      };
+      for (int blk = k_beg; blk < k_end; blk += 64) {
+        load_block<CROSS>(a, s, h, blk + 32, k_beg, k_end, pg_lane, c16, grp, tb);
+        attend(ta, blk);
+        load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
+        attend(tb, blk + 32);
+      }
     }
     if (grp == 0) {
       Pc[c16] = m_run;
