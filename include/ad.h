@@ -140,7 +140,8 @@ typedef struct {
 typedef struct {
   int32_t batch;              /* B >= 1                                              */
   int32_t layout;             /* ad_layout                                           */
-  int32_t k_max;              /* max draft length, 0 <= k_max < max_pos              */
+  int32_t k_max;              /* max draft length, 0 <= k_max < max_pos; bf16 models:
+                                 k_max <= 63 (AD_EUNSUPPORTED otherwise)               */
   int32_t rows;               /* PADDED: B*(k_max+1); PACKED: sum_b (k_b + 1)        */
   const int32_t* tokens;      /* device [rows]: per sequence t0, d_1 .. d_{k_b}      */
   const int32_t* k;           /* device [B]: k_b in [0, k_max]                       */

@@ -387,6 +387,8 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->layout == AD_PACKED && !s->cu_rows) return fail(AD_EINVAL, "packed layout needs cu_rows");
   if (s->batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
   if (s->k_max < 0 || s->k_max + 1 > D.max_pos) return fail(AD_ERANGE, "k_max out of range");
+  if (D.dtype == AD_BF16 && s->k_max + 1 > ad::kMaxBlockRows)
+    return fail(AD_EUNSUPPORTED, "bf16 models verify at most 64 rows per sequence (k_max <= 63)");
   const long long full = (long long)s->batch * (s->k_max + 1);
   if (s->layout == AD_PADDED && s->rows != full)
     return fail(AD_ERANGE, "padded layout needs rows == batch * (k_max + 1)");

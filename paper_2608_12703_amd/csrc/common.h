@@ -151,6 +151,22 @@ __device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
                                    (void __attribute__((address_space(3)))*)lds_wave, 16, 0, 0);
 }
 
+// ----------------------------------------------------------------- split-K sums
+// v[u] = sum over splits t of P[t][e], in split order; the loads of eight splits are
+// issued before their sums.
+__device__ __forceinline__ float4 split_sum4(const float* P, size_t plane, size_t e, int nsplit) {
+  float4 acc = *(const float4*)(P + e);
+  for (int t0 = 1; t0 < nsplit; t0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = *(const float4*)(P + (size_t)min(t0 + u, nsplit - 1) * plane + e);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (t0 + u < nsplit) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
+  }
+  return acc;
+}
+
 // ----------------------------------------------------------------- step descriptors
 // Built by the prep kernel from the caller's device arrays, after validation.
 

@@ -106,6 +106,7 @@ int lm_records(int V);
 constexpr int kAttnPart = 16 + 16 + 64 * 16;   // per chunk: max, sum, O^T (64 x 16)
 constexpr int kSelfChunk = 128;                // keys per wave, self-attention
 constexpr int kCrossChunk = 384;               // frames per wave, cross-attention
+constexpr int kMaxBlockRows = 64;              // bf16 path: rows (k + 1) per sequence
 struct AttnArgs {
   int H, d, layer, cross;
   const SeqDesc* seqs;

@@ -5,7 +5,9 @@
 // partial products; the workgroup finishes them for its head (sum in split order plus
 // bias): the queries go to LDS and, for self-attention, the block's keys and values are
 // rounded to bf16 and written into the paged cache (write-through; commit only moves
-// the cache length) before any wave reads the cache.
+// the cache length).  The waves request their first key blocks before that prologue and
+// do not wait for the cache writes: a self-attention block that reaches the block's own
+// rows takes their keys and values from an LDS copy instead.
 // Scores are computed transposed, S^T = K Q^T (keys on the 16 MFMA rows, queries on the
 // 16 columns), so every lane holds scores of a single query: the online softmax needs
 // only two cross-lane steps and the probabilities are already in the operand order of
@@ -151,11 +153,55 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
   }
 }
 
-__device__ __forceinline__ float finish_proj(const AttnArgs& a, int m, int col) {
-  const size_t plane = (size_t)a.rows * a.qkv_n, e = (size_t)m * a.qkv_n + col;
-  float v = a.qkv_part[e];
-  for (int t = 1; t < a.qkv_splits; ++t) v += a.qkv_part[t * plane + e];
-  return v + bf16_to_f32(a.qkv_bias[col]);
+// Self-attention: replace the keys / values of the block's own rows (positions n ..
+// n + nrows - 1, possibly stale in the loaded tiles) by their LDS copies: nk[r][64]
+// (keys, row-major) and nvt[64][kMaxBlockRows] (values, transposed).
+__device__ __forceinline__ uint4 patch_values(uint4 v, const uint16_t* row, int r0, int nrows) {
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int r = r0 + j;
+    const bool in = r >= 0 && r < nrows;
+    const uint32_t e = row[in ? r : 0];
+    const int sh = (j & 1) * 16;
+    const uint32_t upd = (w[j >> 1] & ~(0xffffu << sh)) | (e << sh);
+    w[j >> 1] = in ? upd : w[j >> 1];
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ uint4 sel4(bool c, uint4 a, uint4 b) {
+  return make_uint4(c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w);
+}
+__device__ __forceinline__ KVTiles patch_new_rows(const KVTiles& t, int blk, int n, int nrows,
+                                                  const uint16_t* nk, const uint16_t* nvt,
+                                                  int c16, int grp) {
+  KVTiles u;
+  const int r = blk + 8 * (c16 >> 2) + (c16 & 3) - n;    // key row of product 0 (+4: product 1)
+  const bool in0 = r >= 0 && r < nrows, in1 = r + 4 >= 0 && r + 4 < nrows;
+  const uint4* s0 = (const uint4*)(nk + (in0 ? r : 0) * kHead + grp * 16);
+  const uint4* s1 = (const uint4*)(nk + (in1 ? r + 4 : 0) * kHead + grp * 16);
+  u.k00 = sel4(in0, s0[0], t.k00);
+  u.k01 = sel4(in0, s0[1], t.k01);
+  u.k10 = sel4(in1, s1[0], t.k10);
+  u.k11 = sel4(in1, s1[1], t.k11);
+  const int r0 = blk + 8 * grp - n;
+  u.v0 = patch_values(t.v0, nvt + (0 * 16 + c16) * kMaxBlockRows, r0, nrows);
+  u.v1 = patch_values(t.v1, nvt + (1 * 16 + c16) * kMaxBlockRows, r0, nrows);
+  u.v2 = patch_values(t.v2, nvt + (2 * 16 + c16) * kMaxBlockRows, r0, nrows);
+  u.v3 = patch_values(t.v3, nvt + (3 * 16 + c16) * kMaxBlockRows, r0, nrows);
+  return u;
+}
+
+// Finish four consecutive columns (col % 4 == 0) of the projection of row m: the split
+// partials summed in split order, plus the bias.
+__device__ __forceinline__ float4 finish_proj4(const AttnArgs& a, int m, int col) {
+  float4 v = split_sum4(a.qkv_part, (size_t)a.rows * a.qkv_n, (size_t)m * a.qkv_n + col, a.qkv_splits);
+  const uint2 bu = *(const uint2*)(a.qkv_bias + col);
+  v.x += bf16_to_f32(bu.x & 0xffff);
+  v.y += bf16_to_f32(bu.x >> 16);
+  v.z += bf16_to_f32(bu.y & 0xffff);
+  v.w += bf16_to_f32(bu.y >> 16);
+  return v;
 }
 
 template <bool CROSS>
@@ -176,37 +222,121 @@ attn_mfma_kernel(AttnArgs a) {
   float* Pc = part + ch * kAttnPart;
   float* qs = part + a.max_chunks * kAttnPart;
 
+  const bool active = ch < n_chunks;
+  // a wave past the last chunk issues the loads of chunk 0 (valid addresses, results
+  // unused): every wave runs the same straight-line prologue, so the compiler keeps
+  // exact outstanding-load counts through it
+  const int k_beg = active ? ch * a.chunk : 0;
+  const int k_end = min(k_beg + a.chunk, n_keys);
+  // self-attention: the chunk's page indices, one per lane (lanes past the chunk repeat
+  // its first page)
+  int pg_lane = 0;
+  if (!CROSS) {
+    const int npg = (k_end - k_beg + kTile - 1) / kTile;
+    const int p = k_beg / kTile + (lane < npg ? lane : 0);
+    pg_lane = min(max(a.block_table[(size_t)b * a.pages_per_seq + p], 0), a.num_pages - 1);
+  }
+  uint16_t* nk = (uint16_t*)(qs + 16 * kHead);   // self: the block rows' keys and values
+  uint16_t* nvt = nk + kMaxBlockRows * kHead;
+  const int nrows = s.k + 1;
+
+  // Prologue loads go out first, as straight-line code: this thread's first query item
+  // and (self) its first block-row item, SP split planes each.  Loads complete in issue
+  // order, so waiting for these later leaves the key loads issued after them in flight.
+  constexpr int SP = CROSS ? 8 : 4;
+  const int S = a.qkv_splits;
+  const size_t plane = (size_t)a.rows * a.qkv_n;
+  const int qr = threadIdx.x >> 4, qj = (threadIdx.x & 15) * 4;        // query item
+  const bool q_on = threadIdx.x < 16 * 16 && qr < nq;
+  const size_t qe = (size_t)(s.row0 + q0 + (q_on ? qr : 0)) * a.qkv_n + h * kHead + qj;
+  const int kr = threadIdx.x >> 5, kkv = (threadIdx.x >> 4) & 1;       // block-row item
+  const bool k_on = !CROSS && (int)threadIdx.x < nrows * 32;
+  const int kcol = a.d + kkv * a.d + h * kHead + qj;
+  const size_t ke = (size_t)(s.row0 + (k_on ? kr : 0)) * a.qkv_n + kcol;
+  float4 qp[SP], kp[SP];
+  uint2 qb, kbias;
+  int kpg = 0;   // page of this thread's block-row item
+#pragma unroll
+  for (int u = 0; u < SP; ++u) qp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + qe);
+  qb = *(const uint2*)(a.qkv_bias + h * kHead + qj);
+  if (!CROSS) {
+#pragma unroll
+    for (int u = 0; u < SP; ++u) kp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + ke);
+    kbias = *(const uint2*)(a.qkv_bias + kcol);
+    const int pos = s.n + (k_on ? kr : 0);
+    kpg = a.block_table[(size_t)b * a.pages_per_seq + pos / kTile];
+  }
+  // keep the key loads below after the prologue loads (issue order is completion order)
+  asm volatile("" ::: "memory");
+  // the first two key blocks
+  KVTiles ta, tb;
+  load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
+  load_block<CROSS>(a, s, h, k_beg + 32, k_beg, k_end, pg_lane, c16, grp, tb);
+  // split sum in split order (planes past SP, if any, in a loop), plus the bias
+  auto finish = [&](const float4 (&pp)[SP], uint2 bu, size_t e) -> float4 {
+    // planes past S add -0, which leaves every value (signed zeros included) unchanged;
+    // no branch, so the loads above stay unconditional
+    float4 v = pp[0];
+#pragma unroll
+    for (int u = 1; u < SP; ++u) {
+      const bool in = u < S;
+      v.x += in ? pp[u].x : -0.f;
+      v.y += in ? pp[u].y : -0.f;
+      v.z += in ? pp[u].z : -0.f;
+      v.w += in ? pp[u].w : -0.f;
+    }
+    for (int t = SP; t < S; ++t) {
+      const float4 w = *(const float4*)(a.qkv_part + (size_t)t * plane + e);
+      v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+    }
+    v.x += bf16_to_f32(bu.x & 0xffff);
+    v.y += bf16_to_f32(bu.x >> 16);
+    v.z += bf16_to_f32(bu.y & 0xffff);
+    v.w += bf16_to_f32(bu.y >> 16);
+    return v;
+  };
+  // the block rows' keys and values: into the cache (bf16) and the LDS copy
+  auto put_kv = [&](int r, int kv, int j, int pg, float4 v) {
+    const int pos = s.n + r;
+    uint16_t* dst = (uint16_t*)a.kv + kv_tile_base(a.layer, kv, pg, h, a.num_pages, a.H);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint16_t e = f32_to_bf16(vv[u]);
+      dst[tile_off(kv, pos % kTile, j + u)] = e;
+      if (kv == 0) nk[r * kHead + j + u] = e;
+      else nvt[(j + u) * kMaxBlockRows + r] = e;
+    }
+  };
+
   // finish the projection: this head's queries of the group, and (self-attention) the
-  // keys / values of every block row of the sequence into the cache
-  for (int idx = threadIdx.x; idx < 16 * kHead; idx += blockDim.x) {
-    const int r = idx >> 6, j = idx & 63;
-    qs[idx] = r < nq ? finish_proj(a, s.row0 + q0 + r, h * kHead + j) : 0.f;
+  // keys / values of every block row of the sequence
+  {
+    const float4 qv = finish(qp, qb, qe);
+    if (threadIdx.x < 16 * 16) *(float4*)(qs + qr * kHead + qj) = q_on ? qv : float4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int idx = threadIdx.x + blockDim.x; idx < 16 * 16; idx += blockDim.x) {   // small blocks
+    const int r = idx >> 4, j = (idx & 15) * 4;
+    *(float4*)(qs + r * kHead + j) =
+        r < nq ? finish_proj4(a, s.row0 + q0 + r, h * kHead + j) : float4{0.f, 0.f, 0.f, 0.f};
   }
   if (!CROSS) {
-    for (int idx = threadIdx.x; idx < (s.k + 1) * 2 * kHead; idx += blockDim.x) {
-      const int r = idx >> 7, kv = (idx >> 6) & 1, j = idx & 63;
-      const float v = finish_proj(a, s.row0 + r, a.d + kv * a.d + h * kHead + j);
+    const float4 kv4 = finish(kp, kbias, ke);
+    if (k_on) put_kv(kr, kkv, qj, min(max(kpg, 0), a.num_pages - 1), kv4);
+    for (int idx = threadIdx.x + blockDim.x; idx < nrows * 32; idx += blockDim.x) {
+      const int r = idx >> 5, kv = (idx >> 4) & 1, j = (idx & 15) * 4;
       const int pos = s.n + r;
-      int pg = a.block_table[(size_t)b * a.pages_per_seq + pos / kTile];
-      pg = min(max(pg, 0), a.num_pages - 1);
-      ((uint16_t*)a.kv)[kv_tile_base(a.layer, kv, pg, h, a.num_pages, a.H) + tile_off(kv, pos % kTile, j)] =
-          f32_to_bf16(v);
+      const int pg = min(max(a.block_table[(size_t)b * a.pages_per_seq + pos / kTile], 0), a.num_pages - 1);
+      put_kv(r, kv, j, pg, finish_proj4(a, s.row0 + r, a.d + kv * a.d + h * kHead + j));
     }
   }
-  __syncthreads();
+  // LDS-only barrier: the key loads above and the cache writes stay in flight
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 
-  if (ch < n_chunks) {
-    const int k_beg = ch * a.chunk, k_end = min(k_beg + a.chunk, n_keys);
+  if (active) {
     const int vis = CROSS ? s.T : s.n + q0 + c16 + 1;
-    // self-attention: the chunk's page indices, one per lane (lanes past the chunk
-    // repeat its first page)
-    int pg_lane = 0;
-    if (!CROSS) {
-      const int npg = (k_end - k_beg + kTile - 1) / kTile;
-      const int p = k_beg / kTile + (lane < npg ? lane : 0);
-      pg_lane = min(max(a.block_table[(size_t)b * a.pages_per_seq + p], 0), a.num_pages - 1);
-    }
-
     // Q^T operand: query c16, dims 16 grp + 8 hh + j, scaled by 1/8 (exact)
     bf16x8 qh[2], ql[2];
     {
@@ -222,22 +352,27 @@ attn_mfma_kernel(AttnArgs a) {
     for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    // ping-pong over 32-key blocks; a block past the chunk end is fully masked and
-    // leaves the state bit-for-bit unchanged
+    // ping-pong over 32-key blocks with the other block's loads in flight; a block past
+    // the chunk end is fully masked and leaves the state bit-for-bit unchanged
     {
-      KVTiles ta, tb;
-      load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
-      // blocks below `clean` need no masking for any query of the group
-      const int clean = CROSS ? k_end : min(k_end, s.n + q0 + 1);
-      auto attend = [&](const KVTiles& t, int blk) {
-        if (blk + 32 <= clean) attend_block<false>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
-        else attend_block<true>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+      // blocks below `clean` need no masking for any query of the group and (self)
+      // hold committed keys only
+      const int clean = CROSS ? k_end : min(k_end, s.n);
+      auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
+        if (blk + 32 <= clean) {
+          attend_block<false>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+        } else if (CROSS) {
+          attend_block<true>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+        } else {
+          attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_end, vis,
+                             grp, qh, ql, o, m_run, l_run);
+        }
       };
       for (int blk = k_beg; blk < k_end; blk += 64) {
-        load_block<CROSS>(a, s, h, blk + 32, k_beg, k_end, pg_lane, c16, grp, tb);
         attend(ta, blk);
         load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
         attend(tb, blk + 32);
+        load_block<CROSS>(a, s, h, blk + 96, k_beg, k_end, pg_lane, c16, grp, tb);
       }
     }
     if (grp == 0) {
@@ -249,7 +384,10 @@ attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) Pc[32 + (dt * 16 + grp * 4 + i) * 16 + c16] = o[dt][i];
   }
-  __syncthreads();
+  // LDS-only barrier (the cache writes need not have landed)
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 
   // merge the chunks in chunk order: output (query qq, dim dd) per thread
   for (int idx = threadIdx.x; idx < 16 * 64; idx += blockDim.x) {
@@ -271,7 +409,8 @@ attn_mfma_kernel(AttnArgs a) {
 
 void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st) {
   const dim3 grid(a.H, B * a.qgroups), block(64 * a.max_chunks);
-  const size_t lds = ((size_t)a.max_chunks * kAttnPart + 16 * kHead) * sizeof(float);
+  const size_t lds = ((size_t)a.max_chunks * kAttnPart + 16 * kHead) * sizeof(float) +
+                     (a.cross ? 0 : 2 * kMaxBlockRows * kHead * sizeof(uint16_t));
   if (a.cross) hipLaunchKernelGGL(attn_mfma_kernel<true>, grid, block, lds, st, a);
   else hipLaunchKernelGGL(attn_mfma_kernel<false>, grid, block, lds, st, a);
 }

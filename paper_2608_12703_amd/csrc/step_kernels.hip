@@ -171,21 +171,6 @@ __device__ __forceinline__ void afrag_store4(uint16_t* base, int RT, int m, int 
       uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
 }
 
-// v[u] = sum over splits t of P[t][e], in split order; the loads of eight splits are
-// issued before their sums.
-__device__ __forceinline__ float4 split_sum4(const float* P, size_t plane, size_t e, int nsplit) {
-  float4 acc = *(const float4*)(P + e);
-  for (int t0 = 1; t0 < nsplit; t0 += 8) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = *(const float4*)(P + (size_t)min(t0 + u, nsplit - 1) * plane + e);
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (t0 + u < nsplit) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
-  }
-  return acc;
-}
-
 // Residual update and the next LayerNorm of one row: x += sum_s P[s] + bias, then
 // LN(x) * g + b goes out in A-fragment order (and to `out` when given).  One thread per
 // 4 columns (blockDim = d / 4 rounded up to whole waves).
