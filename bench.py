@@ -44,6 +44,9 @@ def parse():
     p.add_argument("--layout", default="padded", choices=["padded", "packed"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-kernel-profile", action="store_true")
+    p.add_argument("--copy-calibration-mb", type=int, default=0,
+                   help="after the timed steps, copy a buffer of this many MiB once (a plain "
+                        "copy of known size that calibrates HBM byte counters)")
     return p.parse_args()
 
 
@@ -59,6 +62,25 @@ def gpu_greedy_continuation(sess, t0, ks):
             if it < ks[b]:
                 drafts[b][it] = g[sess.row_of(b, it)]
     return drafts
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cross_attn_{}_traffic.json")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per cross-attention launch from the committed FETCH_SIZE / WRITE_SIZE
+    counter runs (copy-calibrated), or None if there are none for this workload or the
+    kernel's sources changed since they were taken."""
+    from paper_2608_12703_amd.roofline import kernel_source_hash
+    path = TRAFFIC_FILE.format(workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != kernel_source_hash():
+        log("counter traffic is stale (kernel sources changed); traffic = null")
+        return None
+    return rec["hbm_bytes_per_launch"]
 
 
 def cpu_baseline(cfg, params, wl, b=0):
@@ -155,20 +177,38 @@ def main():
     rows = sess.rows
     roof = None
     if not args.no_kernel_profile:
-        # the dominant kernel, timed with HIP events on the step's stream in a second pass
-        ad.profile_enable(sess.model, ad.PROF_CROSS_ATTN, cfg.n_layers * args.steps)
-        for _ in range(args.steps):
-            one_step()
-        tot, n_launch = ad.profile_read(sess.model)
-        ad.profile_enable(sess.model, ad.PROF_CROSS_ATTN, 0)
-        per_launch_s = tot / n_launch / 1e3
+        # The dominant kernel, timed with HIP events on the step's stream over the same
+        # steps.  An event between two kernels delays the next kernel's start by the
+        # launch latency the stream otherwise hides, so events around the kernel alone
+        # overstate it; two passes bracket the kernel before it (the cross-attention
+        # query projection) with and without the cross-attention kernel, and the
+        # difference of the means is the kernel by itself.
+        means = {}
+        for kind in (ad.PROF_XQ_CROSS, ad.PROF_XQ):
+            ad.profile_enable(sess.model, kind, cfg.n_layers * args.steps)
+            for _ in range(args.steps):
+                one_step()
+            tot, n_launch = ad.profile_read(sess.model)
+            means[kind] = tot / n_launch
+        ad.profile_enable(sess.model, ad.PROF_XQ, 0)
+        per_launch_s = (means[ad.PROF_XQ_CROSS] - means[ad.PROF_XQ]) / 1e3
         lb = roofline.cross_attn_launch_bytes(cfg, wl.T, rows)
         achieved = lb / per_launch_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0, "unit": "GB/s",
-                "frac": round(achieved / 8000.0, 4), "traffic": None,
+                "frac": round(achieved / 8000.0, 4), "traffic": measured_traffic(cfg.name),
                 "kernel": "cross_attn", "launch_bytes": lb,
                 "launch_us": round(per_launch_s * 1e6, 2), "launches_timed": n_launch}
         log(f"cross-attention: {per_launch_s * 1e6:.1f} us/launch, {achieved:.0f} GB/s")
+
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {args.copy_calibration_mb} MiB (counter calibration)")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

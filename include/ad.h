@@ -240,11 +240,17 @@ ad_status ad_kv_export(const ad_model* model, const ad_kv* kv, int32_t b, void* 
  * recorded events, returns the summed duration in milliseconds and the number of timed
  * launches, and clears the record.  max_launches = 0 disables timing and frees the
  * events.  Host-side state of the model handle: not thread-safe.
+ * An event recorded between two kernels delays the second one's start by the launch
+ * latency the stream otherwise hides (a few microseconds); the two pair classes bracket
+ * the cross-attention query projection with and without the cross-attention kernel that
+ * follows it, so the difference of their means is that kernel's duration alone.
  */
 #define AD_PROF_CROSS_ATTN 1  /* cross-attention over the encoder K/V              */
 #define AD_PROF_SELF_ATTN 2   /* self-attention over the paged cache               */
 #define AD_PROF_GEMM 3        /* the per-layer projections                         */
 #define AD_PROF_LM_HEAD 4     /* LM head with the fused argmax                     */
+#define AD_PROF_XQ_CROSS 5    /* cross-attention query projection + cross-attention */
+#define AD_PROF_XQ 6          /* cross-attention query projection alone             */
 ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches);
 ad_status ad_profile_read(ad_model* model, double* total_ms, int32_t* launches);
 

@@ -80,7 +80,7 @@ EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model
            "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_profile_enable", "ad_profile_read")
-PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD = 1, 2, 3, 4
+PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD, PROF_XQ_CROSS, PROF_XQ = 1, 2, 3, 4, 5, 6
 
 
 class ADError(RuntimeError):

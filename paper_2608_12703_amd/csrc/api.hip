@@ -104,6 +104,8 @@ ad_status check_hip(const char* where) {
 }
 
 // Brackets one kernel launch with a profiling event pair when that class is enabled.
+// Timing of the selected kernel class: a start / stop event pair on the stream around
+// its launch (or, for the pair classes, around a short sequence of launches).
 struct ProfScope {
   ad_model* m;
   hipStream_t st;
@@ -115,9 +117,11 @@ struct ProfScope {
       (void)hipEventRecord(m->prof_start[idx], st);
     }
   }
-  ~ProfScope() {
+  void stop() {
     if (idx >= 0) (void)hipEventRecord(m->prof_stop[idx], st);
+    idx = -1;
   }
+  ~ProfScope() { stop(); }
 };
 
 template <class S>
@@ -228,8 +232,13 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_O), none, AD_PROF_GEMM);
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_O), w.x,
                              lp(m, l, LN2_G), lp(m, l, LN2_B), w.afrag, RT, nullptr, st);
-    // cross-attention sublayer
-    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XQ), none, AD_PROF_GEMM);
+    // cross-attention sublayer (the pair classes time the query projection with and
+    // without the attention after it: their difference is the attention kernel alone)
+    ProfScope xq_cross(m, AD_PROF_XQ_CROSS, st);
+    {
+      ProfScope xq(m, AD_PROF_XQ, st);
+      gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XQ), none, AD_PROF_GEMM);
+    }
     at.cross = 1; at.kv = (const uint16_t*)s->cross.data; at.chunk = ad::kCrossChunk;
     at.max_chunks = div_up(D.max_frames, ad::kCrossChunk);
     at.qkv_splits = ad::gemm_splits(d, d); at.qkv_n = d;
@@ -238,6 +247,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
       ad::launch_attn_mfma(at, s->batch, st);
     }
+    xq_cross.stop();
     gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XO), none, AD_PROF_GEMM);
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_XO), w.x,
                              lp(m, l, LN3_G), lp(m, l, LN3_B), w.afrag, RT, nullptr, st);
@@ -332,15 +342,17 @@ ad_status ad_model_destroy(ad_model* model) {
 ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches) {
   if (!model) return fail(AD_EINVAL, "model is NULL");
   if (max_launches < 0 || max_launches > (1 << 20)) return fail(AD_ERANGE, "max_launches out of range");
-  if (max_launches > 0 && (kernel < AD_PROF_CROSS_ATTN || kernel > AD_PROF_LM_HEAD))
+  if (max_launches > 0 && (kernel < AD_PROF_CROSS_ATTN || kernel > AD_PROF_XQ))
     return fail(AD_EINVAL, "unknown kernel class");
   prof_free(model);
   if (max_launches == 0) return AD_OK;
   model->prof_start.resize(max_launches);
   model->prof_stop.resize(max_launches);
   for (int i = 0; i < max_launches; ++i) {
-    if (hipEventCreate(&model->prof_start[i]) != hipSuccess ||
-        hipEventCreate(&model->prof_stop[i]) != hipSuccess) {
+    // no system-scope fence: a default event record releases (writes back) the caches,
+    // which would stall the timed kernel and inflate its measured duration
+    if (hipEventCreateWithFlags(&model->prof_start[i], hipEventDisableSystemFence) != hipSuccess ||
+        hipEventCreateWithFlags(&model->prof_stop[i], hipEventDisableSystemFence) != hipSuccess) {
       model->prof_start.resize(i);
       model->prof_stop.resize(i);
       prof_free(model);

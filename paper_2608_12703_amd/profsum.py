@@ -1,0 +1,90 @@
+"""Summaries of rocprofv3 result databases (SQLite, ROCm 7).
+
+  python -m paper_2608_12703_amd.profsum kernels RESULTS.db [--calls N] [--command CMD]
+      per-kernel dispatch count, mean / min / max duration and share of GPU time
+      (--calls: divide the totals by this many verify steps)
+  python -m paper_2608_12703_amd.profsum traffic --fetch FETCH.db --write WRITE.db
+          --kernel NAME --calib-mib MIB --out OUT.json [--command CMD]
+      HBM bytes per dispatch of one kernel from a FETCH_SIZE run and a WRITE_SIZE run,
+      each scaled by what the same counter reads for a plain copy of MIB MiB captured in
+      the same run (the largest copyBuffer dispatch)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sqlite3
+import sys
+
+from .roofline import kernel_source_hash
+
+
+def kernel_table(db: str, calls: int | None = None) -> str:
+    cur = sqlite3.connect(db).cursor()
+    rows = cur.execute("select name, count(*), avg(end - start), min(end - start), max(end - start), "
+                       "sum(end - start) from kernels group by name order by sum(end - start) desc").fetchall()
+    total = sum(r[5] for r in rows) or 1
+    out = [f"{'kernel':70s} {'calls':>7s} {'mean us':>9s} {'min us':>9s} {'max us':>9s} {'share':>6s}"
+           + (f" {'us/step':>9s}" if calls else "")]
+    for name, n, avg, mn, mx, tot in rows:
+        line = f"{name[:70]:70s} {n:7d} {avg / 1e3:9.2f} {mn / 1e3:9.2f} {mx / 1e3:9.2f} {100 * tot / total:5.1f}%"
+        if calls:
+            line += f" {tot / 1e3 / calls:9.1f}"
+        out.append(line)
+    return "\n".join(out)
+
+
+def _counter(db: str, kernel: str):
+    cur = sqlite3.connect(db).cursor()
+    vals = [r[0] for r in cur.execute("select value from counters_collection where kernel_name like ?",
+                                      (f"%{kernel}%",))]
+    copies = [r[0] for r in cur.execute("select value from counters_collection where kernel_name like "
+                                        "'%copyBuffer%'")]
+    if not vals or not copies:
+        raise SystemExit(f"{db}: no dispatches of {kernel!r} or of the calibration copy")
+    return sum(vals) / len(vals), len(vals), max(copies)
+
+
+def traffic(fetch_db: str, write_db: str, kernel: str, calib_mib: int, command: str) -> dict:
+    f_kib, f_n, f_copy = _counter(fetch_db, kernel)
+    w_kib, w_n, w_copy = _counter(write_db, kernel)
+    known_kib = calib_mib * 1024.0
+    f_scale, w_scale = known_kib / f_copy, known_kib / w_copy
+    return {"kernel": kernel, "source_sha256": kernel_source_hash(),
+            "fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1),
+            "dispatches": [f_n, w_n],
+            "calibration": {"copy_mib": calib_mib, "fetch_kib": f_copy, "write_kib": w_copy,
+                            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+            "hbm_bytes_per_launch": int(round((f_kib * f_scale + w_kib * w_scale) * 1024)),
+            "command": command}
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser(prog="profsum")
+    sub = p.add_subparsers(dest="cmd", required=True)
+    k = sub.add_parser("kernels")
+    k.add_argument("db")
+    k.add_argument("--calls", type=int)
+    k.add_argument("--command", default="")
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--kernel", required=True)
+    t.add_argument("--calib-mib", type=int, required=True)
+    t.add_argument("--out", required=True)
+    t.add_argument("--command", default="")
+    a = p.parse_args(argv)
+    if a.cmd == "kernels":
+        if a.command:
+            print(f"command: {a.command}\n")
+        print(kernel_table(a.db, a.calls))
+    else:
+        rec = traffic(a.fetch, a.write, a.kernel, a.calib_mib, a.command)
+        with open(a.out, "w") as fh:
+            json.dump(rec, fh, indent=1)
+        json.dump(rec, sys.stdout, indent=1)
+        print()
+
+
+if __name__ == "__main__":
+    main()

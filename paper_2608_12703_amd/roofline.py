@@ -10,6 +10,9 @@ Activations (float32 rows, < 1% at the large shapes) are counted per kernel belo
 """
 from __future__ import annotations
 
+import hashlib
+import os
+
 import numpy as np
 
 HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
@@ -46,3 +49,17 @@ def step_flops(cfg, n, T, k) -> dict:
     M = int(np.sum(k + 1))
     return {"gemm": 2 * (L * (6 * d * d + 2 * d * F) + V * d) * M,
             "attention": int(np.sum(4 * (k + 1) * (T + n + k + 1) * d * L))}
+
+
+# Sources the cross-attention kernel is built from; HBM counter figures taken for one
+# version of them are reported only while they are unchanged.
+_CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+KERNEL_SOURCES = ("mfma_attn.hip", "common.h", "launch.h")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(_CSRC, name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
