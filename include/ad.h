@@ -107,6 +107,21 @@ ad_status ad_model_create(const ad_model_desc* desc, const void* const* params,
 ad_status ad_model_destroy(ad_model* model);
 
 /*
+ * Optional weight tiling for the bf16 matrix-core path.  ad_model_pack_size gives the
+ * bytes of a caller-allocated device buffer; ad_model_pack fills it with a tiled copy of
+ * every projection matrix and of the tied LM head (for each 128-column tile and 32-wide
+ * K step, one contiguous 8 KB block in the order the kernels stage it) and makes the
+ * model read its weights from there.  The buffer must stay allocated and unchanged while
+ * the model is used; pack again after changing the parameters.  buffer = NULL returns
+ * the model to its row-major parameters.  Results are bit-identical either way; the
+ * tiled copy streams from HBM in whole contiguous blocks.
+ * Errors: AD_EINVAL (NULL model, buffer not 256-byte aligned), AD_ENOSPACE (bytes too
+ * small), AD_EUNSUPPORTED (float32 model).
+ */
+ad_status ad_model_pack_size(const ad_model* model, size_t* bytes);
+ad_status ad_model_pack(ad_model* model, void* buffer, size_t bytes, void* stream);
+
+/*
  * Paged self-attention KV cache.  pool holds
  *   n_layers * 2 * num_pages * n_heads * 16 * 64 elements of the model dtype
  * arranged as [layer][K|V][page][head][16-token tile]; the element order inside a tile

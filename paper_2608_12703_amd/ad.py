@@ -57,6 +57,8 @@ def _load():
         "ad_model_create": (_i32, [ctypes.POINTER(ModelDesc), ctypes.POINTER(_ptr), _i32,
                                    ctypes.POINTER(_ptr)]),
         "ad_model_destroy": (_i32, [_ptr]),
+        "ad_model_pack_size": (_i32, [_ptr, ctypes.POINTER(_size)]),
+        "ad_model_pack": (_i32, [_ptr, _ptr, _size, _ptr]),
         "ad_workspace_size": (_i32, [_ptr, _i32, _i32, _i32, ctypes.POINTER(_size)]),
         "ad_cross_kv_prefill": (_i32, [_ptr, _ptr, ctypes.POINTER(Cross), _ptr]),
         "ad_verify_step": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
@@ -77,6 +79,7 @@ def _load():
 
 LIB = _load()
 EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model_destroy",
+           "ad_model_pack_size", "ad_model_pack",
            "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_profile_enable", "ad_profile_read")
@@ -132,6 +135,19 @@ class Model:
         check(LIB.ad_workspace_size(self.handle, rows, batch, k_max, ctypes.byref(n)),
               "ad_workspace_size")
         return n.value
+
+    def pack_size(self) -> int:
+        n = _size()
+        check(LIB.ad_model_pack_size(self.handle, ctypes.byref(n)), "ad_model_pack_size")
+        return n.value
+
+    def pack(self, buffer, stream=None):
+        """Tile the weights into `buffer` (a device tensor of at least pack_size() bytes,
+        kept alive here), or return to the row-major parameters with buffer=None."""
+        check(LIB.ad_model_pack(self.handle, ptr(buffer), 0 if buffer is None else
+                                buffer.numel() * buffer.element_size(), stream_handle(stream)),
+              "ad_model_pack")
+        self.packed = buffer
 
     def draft_heads_workspace_size(self, n_heads: int, batch: int) -> int:
         n = _size()

@@ -11,6 +11,8 @@
 struct ad_model {
   ad_model_desc desc;
   std::vector<const void*> p;
+  const uint16_t* packed = nullptr;   // tiled weights (ad_model_pack), or NULL
+  std::vector<size_t> pack_off;       // their element offsets (packed_offsets)
   // launch timing (ad_profile_enable / ad_profile_read)
   int prof_kernel = 0;
   std::vector<hipEvent_t> prof_start, prof_stop;
@@ -36,6 +38,35 @@ enum LayerParam {
 
 const void* lp(const ad_model* m, int layer, int which) {
   return m->p[4 + layer * N_LAYER_PARAMS + which];
+}
+
+// Tiled-weight buffer: per layer W_QKV, W_O, W_XQ, W_XO, W_1, W_2, then the LM head.
+constexpr int kPackedPerLayer = 6;
+const int kPackedWhich[kPackedPerLayer] = {W_QKV, W_O, W_XQ, W_XO, W_1, W_2};
+
+void packed_shape(const ad_model_desc& D, int which, int& N, int& K) {
+  const int d = D.d_model, F = D.d_ffn;
+  N = d; K = d;
+  if (which == W_QKV) N = 3 * d;
+  if (which == W_1) N = F;
+  if (which == W_2) K = F;
+}
+
+// element offsets of every tiled matrix (index layer * 6 + slot; the LM head last)
+std::vector<size_t> packed_offsets(const ad_model_desc& D) {
+  std::vector<size_t> off;
+  size_t o = 0;
+  for (int l = 0; l < D.n_layers; ++l)
+    for (int j = 0; j < kPackedPerLayer; ++j) {
+      int N, K;
+      packed_shape(D, kPackedWhich[j], N, K);
+      off.push_back(o);
+      o += (ad::packed_weight_elems(N, K) + 127) / 128 * 128;   // 256-byte aligned
+    }
+  off.push_back(o);
+  o += (ad::packed_weight_elems(D.vocab, D.d_model) + 127) / 128 * 128;
+  off.push_back(o);   // total
+  return off;
 }
 
 // Workspace carve-up for a step with M rows and B sequences.
@@ -87,8 +118,9 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
     w.afrag = (uint16_t*)take(4ull * Mp * D);
     w.hfrag = (uint16_t*)take(4ull * Mp * F);
     size_t gp = 0;
-    const int shapes[6][2] = {{3 * (int)D, (int)D}, {(int)D, (int)D}, {(int)D, (int)D},
-                              {(int)D, (int)D}, {(int)F, (int)D}, {(int)D, (int)F}};
+    // projections that leave split-K partials (the FFN up-projection does not)
+    const int shapes[5][2] = {{3 * (int)D, (int)D}, {(int)D, (int)D}, {(int)D, (int)D},
+                              {(int)D, (int)D}, {(int)D, (int)F}};
     for (auto& sh : shapes) gp = std::max(gp, ad::gemm_part_floats(M, sh[0], sh[1]));
     w.gpart = (float*)take(4 * gp);
     w.ampart = take(16ull * M * ad::lm_records((int)V));
@@ -187,9 +219,10 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
 }
 
-// bf16 model.  Every projection writes split-K partial products; the next kernel
-// finishes them: the attention kernels (queries, and the block's keys / values into the
-// cache), the residual + LayerNorm row kernel, or the GELU reduction.
+// bf16 model.  The projections write split-K partial products that the next kernel
+// finishes: the attention kernels (queries, and the block's keys / values into the
+// cache) or the residual + LayerNorm row kernel.  The FFN up-projection runs unsplit with
+// bias + GELU in its epilogue.
 void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
   const ad_model_desc& D = m->desc;
   const int M = s->rows, d = D.d_model, F = D.d_ffn, H = D.n_heads, V = D.vocab, RT = w.RT;
@@ -201,10 +234,21 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::launch_embed_ln(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, lp(m, 0, LN1_G), lp(m, 0, LN1_B),
                       w.afrag, RT, st);
 
-  auto gemm = [&](int epi, int N, int K, const uint16_t* A, const void* W, ad::EpiArgs e, int prof) {
+  const std::vector<size_t>& poff = m->pack_off;
+  // weight `which` of layer l (layer -1: the LM head), tiled when the model is packed
+  auto wt = [&](int l, int which, const void* rowmajor, int& packed) -> const uint16_t* {
+    packed = m->packed != nullptr;
+    if (!packed) return (const uint16_t*)rowmajor;
+    if (l < 0) return m->packed + poff[D.n_layers * kPackedPerLayer];
+    const int slot = (int)(std::find(kPackedWhich, kPackedWhich + kPackedPerLayer, which) - kPackedWhich);
+    return m->packed + poff[l * kPackedPerLayer + slot];
+  };
+  auto gemm = [&](int epi, int N, int K, const uint16_t* A, int l, int which, ad::EpiArgs e,
+                  int prof, const void* bias = nullptr) {
     ad::GemmArgs g{};
     g.M = M; g.N = N; g.K = K; g.RT = RT; g.A = A;
-    g.W = (const uint16_t*)W;
+    g.W = wt(l, which, l < 0 ? m->p[P_TOK] : lp(m, l, which), g.packed);
+    g.bias = (const uint16_t*)bias;
     g.part = w.gpart;
     g.e = e;
     ProfScope ps(m, prof, st);
@@ -220,7 +264,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   for (int l = 0; l < D.n_layers; ++l) {
     at.layer = l;
     // self-attention sublayer (LN1 was applied by the previous row kernel)
-    gemm(ad::EPI_PARTIAL, 3 * d, d, w.afrag, lp(m, l, W_QKV), none, AD_PROF_GEMM);
+    gemm(ad::EPI_PARTIAL, 3 * d, d, w.afrag, l, W_QKV, none, AD_PROF_GEMM);
     at.cross = 0; at.kv = (const uint16_t*)s->kv.pool; at.chunk = ad::kSelfChunk;
     at.max_chunks = div_up(D.max_pos, ad::kSelfChunk);
     at.qkv_splits = ad::gemm_splits(3 * d, d); at.qkv_n = 3 * d;
@@ -229,7 +273,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
       ProfScope ps(m, AD_PROF_SELF_ATTN, st);
       ad::launch_attn_mfma(at, s->batch, st);
     }
-    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_O), none, AD_PROF_GEMM);
+    gemm(ad::EPI_PARTIAL, d, d, w.afrag, l, W_O, none, AD_PROF_GEMM);
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_O), w.x,
                              lp(m, l, LN2_G), lp(m, l, LN2_B), w.afrag, RT, nullptr, st);
     // cross-attention sublayer (the pair classes time the query projection with and
@@ -237,7 +281,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     ProfScope xq_cross(m, AD_PROF_XQ_CROSS, st);
     {
       ProfScope xq(m, AD_PROF_XQ, st);
-      gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XQ), none, AD_PROF_GEMM);
+      gemm(ad::EPI_PARTIAL, d, d, w.afrag, l, W_XQ, none, AD_PROF_GEMM);
     }
     at.cross = 1; at.kv = (const uint16_t*)s->cross.data; at.chunk = ad::kCrossChunk;
     at.max_chunks = div_up(D.max_frames, ad::kCrossChunk);
@@ -248,19 +292,16 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
       ad::launch_attn_mfma(at, s->batch, st);
     }
     xq_cross.stop();
-    gemm(ad::EPI_PARTIAL, d, d, w.afrag, lp(m, l, W_XO), none, AD_PROF_GEMM);
+    gemm(ad::EPI_PARTIAL, d, d, w.afrag, l, W_XO, none, AD_PROF_GEMM);
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_XO), w.x,
                              lp(m, l, LN3_G), lp(m, l, LN3_B), w.afrag, RT, nullptr, st);
     // feed-forward sublayer
-    gemm(ad::EPI_PARTIAL, F, d, w.afrag, lp(m, l, W_1), none, AD_PROF_GEMM);
     {
-      ad::GemmArgs g{};
-      g.M = M; g.N = F; g.K = d; g.RT = RT; g.part = w.gpart;
-      g.bias = (const uint16_t*)lp(m, l, B_1);
-      g.e.frag = w.hfrag; g.e.frag_RT = RT;
-      ad::launch_gelu_reduce(g, st);
+      ad::EpiArgs e{};
+      e.frag = w.hfrag; e.frag_RT = RT;
+      gemm(ad::EPI_GELU, F, d, w.afrag, l, W_1, e, AD_PROF_GEMM, lp(m, l, B_1));
     }
-    gemm(ad::EPI_PARTIAL, d, F, w.hfrag, lp(m, l, W_2), none, AD_PROF_GEMM);
+    gemm(ad::EPI_PARTIAL, d, F, w.hfrag, l, W_2, none, AD_PROF_GEMM);
     const bool last = l + 1 == D.n_layers;
     float* hidden = s->out_hidden ? s->out_hidden : w.hidden;
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, F), w.gpart, lp(m, l, B_2), w.x,
@@ -270,7 +311,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   }
   ad::EpiArgs e{};
   e.out = s->out_logits; e.ldo = V; e.am_part = w.ampart;
-  gemm(ad::EPI_ARGMAX, V, d, w.afrag, m->p[P_TOK], e, AD_PROF_LM_HEAD);
+  gemm(ad::EPI_ARGMAX, V, d, w.afrag, -1, 0, e, AD_PROF_LM_HEAD);
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
   ad::launch_argmax_final(M, ad::lm_records(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
@@ -331,6 +372,45 @@ static void prof_free(ad_model* m) {
   m->prof_stop.clear();
   m->prof_used = 0;
   m->prof_kernel = 0;
+}
+
+ad_status ad_model_pack_size(const ad_model* model, size_t* bytes) {
+  if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
+  if (model->desc.dtype != AD_BF16) return fail(AD_EUNSUPPORTED, "weight tiling is for bf16 models");
+  *bytes = packed_offsets(model->desc).back() * sizeof(uint16_t);
+  return AD_OK;
+}
+
+ad_status ad_model_pack(ad_model* model, void* buffer, size_t bytes, void* stream) {
+  if (!model) return fail(AD_EINVAL, "model is NULL");
+  if (model->desc.dtype != AD_BF16) return fail(AD_EUNSUPPORTED, "weight tiling is for bf16 models");
+  if (!buffer) {
+    model->packed = nullptr;
+    model->pack_off.clear();
+    return AD_OK;
+  }
+  if ((uintptr_t)buffer % 256) return fail(AD_EINVAL, "pack buffer must be 256-byte aligned");
+  const ad_model_desc& D = model->desc;
+  const std::vector<size_t> off = packed_offsets(D);
+  if (bytes < off.back() * sizeof(uint16_t))
+    return fail(AD_ENOSPACE, "pack buffer needs " + std::to_string(off.back() * sizeof(uint16_t)) + " bytes");
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  uint16_t* P = (uint16_t*)buffer;
+  for (int l = 0; l < D.n_layers; ++l)
+    for (int j = 0; j < kPackedPerLayer; ++j) {
+      int N, K;
+      packed_shape(D, kPackedWhich[j], N, K);
+      ad::launch_pack_weight((const uint16_t*)lp(model, l, kPackedWhich[j]), N, K,
+                             P + off[l * kPackedPerLayer + j], st);
+    }
+  ad::launch_pack_weight((const uint16_t*)model->p[P_TOK], D.vocab, D.d_model,
+                         P + off[D.n_layers * kPackedPerLayer], st);
+  const ad_status rc = check_hip("ad_model_pack");
+  if (rc != AD_OK) return rc;
+  model->packed = P;
+  model->pack_off = off;
+  return AD_OK;
 }
 
 ad_status ad_model_destroy(ad_model* model) {

@@ -83,18 +83,22 @@ void launch_gemm_valu_bf16a(int epi, int M, int N, int K, const void* A, const v
 struct GemmArgs {
   int M, N, K, RT;
   const uint16_t* A;
-  const uint16_t* W;
+  const uint16_t* W;     // [N][K] row-major, or tiled by pack_weight (packed = 1)
+  int packed;
   const uint16_t* bias;
   int S, KB, ntiles, mchunks;  // set by the launcher
   float* part;           // split-K partial products [S][M][N]
   EpiArgs e;
 };
-// epi = EPI_PARTIAL (split-K partial products into `part`) or EPI_ARGMAX (LM head:
-// per-tile top-2 records into e.am_part, optional logits into e.out).
+// epi = EPI_PARTIAL (split-K partial products into `part`), EPI_GELU (unsplit; bias +
+// GELU into e.frag in A-fragment order) or EPI_ARGMAX (LM head: per-tile top-2 records
+// into e.am_part, optional logits into e.out).
 void launch_gemm_mfma(int epi, GemmArgs g, hipStream_t st);
-// Sum the split-K partials of a preceding EPI_PARTIAL launch, add the bias, apply GELU and
-// store the result in A-fragment order (e.frag, e.frag_RT).
-void launch_gelu_reduce(GemmArgs g, hipStream_t st);
+// Weight tiling read by the matrix-core GEMM: for each 128-column tile and 32-wide K step
+// one contiguous 8 KB stage, in the order the kernel stages it (column tile, lane, 8 k).
+// Columns past N are zero.  Elements of the tiled copy of an N x K matrix:
+size_t packed_weight_elems(int N, int K);
+void launch_pack_weight(const uint16_t* W, int N, int K, uint16_t* P, hipStream_t st);
 void launch_argmax_final(int M, int nrec, const void* part, const RowDesc* rows, int* greedy,
                          float* margin, int* err, hipStream_t st);
 int gemm_splits(int N, int K);

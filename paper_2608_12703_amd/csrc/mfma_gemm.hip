@@ -103,13 +103,15 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][4], const uint4* 
   }
 }
 
-template <int EPI, int RTC>
+template <int EPI, int RTC, bool PACKED>
 __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   constexpr int RW = RTC / 4;            // row tiles per wave
   constexpr int NA = RTC / 4;            // direct loads per wave for one activation stage
   // Activation ring: 3 stages (requested 2 steps ahead); weight ring: 6 stages (requested
   // 5 steps ahead, covering HBM latency).  Distinct LDS objects, so the compiler can tell
-  // a read of one stage from the direct loads still filling another.
+  // a read of one stage from the direct loads still filling another.  (Measured slower:
+  // a 12-stage weight ring, and 6-stage rings for both operands; larger LDS footprints
+  // cost more than the deeper prefetch gains.)
   __shared__ uint4 sa0[RTC * 128], sa1[RTC * 128], sa2[RTC * 128];
   __shared__ uint4 sw0[512], sw1[512], sw2[512], sw3[512], sw4[512], sw5[512];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -145,45 +147,51 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   };
   auto iw = [&](uint4* buf, int kb) {   // weight stage of step kb (clamped)
     const int k = min(kb, kl);
-    const int n = min(n0 + w * 16 + (lane & 15), g.N - 1);   // column tile w
-    dma16(g.W + (size_t)n * g.K + k * 32 + (lane >> 4) * 8, buf + w * 64);
+    if constexpr (PACKED) {              // one contiguous 8 KB stage
+      dma16(g.W + ((size_t)(nt * g.KB + k) * 512 + w * 64 + lane) * 8, buf + w * 64);
+    } else {
+      const int n = min(n0 + w * 16 + (lane & 15), g.N - 1);   // column tile w
+      dma16(g.W + (size_t)n * g.K + k * 32 + (lane >> 4) * 8, buf + w * 64);
+    }
   };
-  // Step j requests activations j + 2 and weights j + 5, in that order; the prologue
-  // plays virtual steps -5 .. -1 so the outstanding-load count is the same everywhere:
-  // at the end of step j the loads issued after A(j+1) are W(j+4), A(j+2), W(j+5).
-  constexpr int kWaitAfter = NA + 2;
-  iw(sw0, kb0);
-  iw(sw1, kb0 + 1);
-  iw(sw2, kb0 + 2);
-  ia(sa0, kb0);
-  iw(sw3, kb0 + 3);
-  ia(sa1, kb0 + 1);
-  iw(sw4, kb0 + 4);
-  BARRIER_VMCNT(kWaitAfter);
   int kb = kb0;
+  {
+    // Step j requests activations j + 2 and weights j + 5, in that order; the prologue
+    // plays virtual steps -5 .. -1 so the outstanding-load count is the same everywhere:
+    // at the end of step j the loads issued after A(j+1) are W(j+4), A(j+2), W(j+5).
+    constexpr int kWait = NA + 2;
+    iw(sw0, kb0);
+    iw(sw1, kb0 + 1);
+    iw(sw2, kb0 + 2);
+    ia(sa0, kb0);
+    iw(sw3, kb0 + 3);
+    ia(sa1, kb0 + 1);
+    iw(sw4, kb0 + 4);
+    BARRIER_VMCNT(kWait);
 #define GEMM_STEP(CA, CW, NXA, NXW)            \
   {                                            \
     ia(NXA, kb + 2);                           \
     iw(NXW, kb + 5);                           \
     mma_step<RTC>(acc, CA, CW, rg, ch, lane);  \
-    BARRIER_VMCNT(kWaitAfter);                 \
+    BARRIER_VMCNT(kWait);                      \
     ++kb;                                      \
   }
-  for (int it = 0; it < nk / 6; ++it) {
-    GEMM_STEP(sa0, sw0, sa2, sw5)
-    GEMM_STEP(sa1, sw1, sa0, sw0)
-    GEMM_STEP(sa2, sw2, sa1, sw1)
-    GEMM_STEP(sa0, sw3, sa2, sw2)
-    GEMM_STEP(sa1, sw4, sa0, sw3)
-    GEMM_STEP(sa2, sw5, sa1, sw4)
-  }
-  const int rem = nk % 6;
-  if (rem >= 1) GEMM_STEP(sa0, sw0, sa2, sw5)
-  if (rem >= 2) GEMM_STEP(sa1, sw1, sa0, sw0)
-  if (rem >= 3) GEMM_STEP(sa2, sw2, sa1, sw1)
-  if (rem >= 4) GEMM_STEP(sa0, sw3, sa2, sw2)
-  if (rem >= 5) GEMM_STEP(sa1, sw4, sa0, sw3)
+    for (int it = 0; it < nk / 6; ++it) {
+      GEMM_STEP(sa0, sw0, sa2, sw5)
+      GEMM_STEP(sa1, sw1, sa0, sw0)
+      GEMM_STEP(sa2, sw2, sa1, sw1)
+      GEMM_STEP(sa0, sw3, sa2, sw2)
+      GEMM_STEP(sa1, sw4, sa0, sw3)
+      GEMM_STEP(sa2, sw5, sa1, sw4)
+    }
+    const int rem = nk % 6;
+    if (rem >= 1) GEMM_STEP(sa0, sw0, sa2, sw5)
+    if (rem >= 2) GEMM_STEP(sa1, sw1, sa0, sw0)
+    if (rem >= 3) GEMM_STEP(sa2, sw2, sa1, sw1)
+    if (rem >= 4) GEMM_STEP(sa0, sw3, sa2, sw2)
+    if (rem >= 5) GEMM_STEP(sa1, sw4, sa0, sw3)
 #undef GEMM_STEP
+  }
   BARRIER_VMCNT(0);
 
   // row / column of accumulator element (r, ct, i) of this lane
@@ -239,6 +247,30 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     return;
   }
 
+  if (EPI == EPI_GELU) {
+    // FFN up-projection (unsplit): bias + GELU, stored straight from registers as the
+    // next product's A operand (hi/lo bf16 pair in A-fragment order)
+    float bv[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const int n = min(col_base + ct * 16, g.N - 1);
+      bv[ct] = bf16_to_f32(g.bias[n]);
+    }
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = row_base + r * 16 + i;
+        if (m >= g.M) continue;
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+          const int n = col_base + ct * 16;
+          if (n < g.N) afrag_store(g.e.frag, g.e.frag_RT, m, n, gelu_erf(acc[r][ct][i] + bv[ct]));
+        }
+      }
+    return;
+  }
+
   // EPI_PARTIAL: the raw split-K partial product straight from registers (16 lanes store
   // 64 contiguous bytes of a row); the consumer kernel sums the splits in split order.
   float* P = g.part + (size_t)s * g.M * g.N;
@@ -256,35 +288,17 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     }
 }
 
-// FFN up-projection epilogue: sum the S partial products of each element in split
-// order, add the bias, apply GELU and store the result as the next product's A operand.
-// One thread per 4 consecutive columns; the loads of eight splits are issued before
-// their sums.
-__global__ void __launch_bounds__(256) gelu_reduce_kernel(GemmArgs g) {
-  const int n4 = g.N / 4;
-  const size_t total4 = (size_t)g.M * n4, plane = (size_t)g.M * g.N;
-  for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < total4; q += (size_t)gridDim.x * 256) {
-    const int m = (int)(q / n4), n = (int)(q % n4) * 4;
-    const size_t e = (size_t)m * g.N + n;
-    float4 acc = *(const float4*)(g.part + e);
-    for (int t0 = 1; t0 < g.S; t0 += 8) {
-      float4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = *(const float4*)(g.part + (size_t)min(t0 + u, g.S - 1) * plane + e);
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (t0 + u < g.S) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
-    }
-    const uint2 bu = *(const uint2*)(g.bias + n);
-    float y[4] = {gelu_erf(acc.x + bf16_to_f32(bu.x & 0xffff)), gelu_erf(acc.y + bf16_to_f32(bu.x >> 16)),
-                  gelu_erf(acc.z + bf16_to_f32(bu.y & 0xffff)), gelu_erf(acc.w + bf16_to_f32(bu.y >> 16))};
-    uint16_t h[4], l[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) split_hilo(y[i], h[i], l[i]);
-    *(uint2*)(g.e.frag + afrag_index(m, n, 0, g.e.frag_RT)) =
-        uint2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
-    *(uint2*)(g.e.frag + afrag_index(m, n, 1, g.e.frag_RT)) =
-        uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
+// Tiled weight copy (see launch.h): one thread per 16-byte piece.
+__global__ void __launch_bounds__(256) pack_weight_kernel(const uint16_t* W, int N, int K,
+                                                          uint16_t* P, size_t pieces) {
+  const int KB = K / 32;
+  for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < pieces; q += (size_t)gridDim.x * 256) {
+    const size_t stage = q / 512;
+    const int t = (int)(q % 512), ct = t / 64, lane = t % 64;
+    const int nt = (int)(stage / KB), kb = (int)(stage % KB);
+    const int n = nt * kNT + ct * 16 + (lane & 15), k = kb * 32 + (lane >> 4) * 8;
+    const uint4 v = n < N ? *(const uint4*)(W + (size_t)n * K + k) : make_uint4(0, 0, 0, 0);
+    *(uint4*)(P + q * 8) = v;
   }
 }
 
@@ -346,6 +360,14 @@ int gemm_rtc(int M, int N, int S) {
 
 size_t gemm_part_floats(int M, int N, int K) { return (size_t)gemm_splits(N, K) * M * N; }
 
+size_t packed_weight_elems(int N, int K) { return (size_t)((N + kNT - 1) / kNT) * kNT * K; }
+
+void launch_pack_weight(const uint16_t* W, int N, int K, uint16_t* P, hipStream_t st) {
+  const size_t pieces = packed_weight_elems(N, K) / 8;
+  const dim3 grid((unsigned)std::min<size_t>((pieces + 255) / 256, 8192)), block(256);
+  hipLaunchKernelGGL(pack_weight_kernel, grid, block, 0, st, W, N, K, P, pieces);
+}
+
 int lm_records(int V) { return 2 * ((V + kNT - 1) / kNT); }
 
 template <int EPI>
@@ -353,27 +375,31 @@ static void launch_one(GemmArgs g, hipStream_t st) {
   const int rtc = gemm_rtc(g.M, g.N, g.S);
   g.mchunks = mchunks_of(g.M, rtc);
   const dim3 grid(g.ntiles * g.S * g.mchunks), block(512);
-  if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4>), grid, block, 0, st, g);
-  else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8>), grid, block, 0, st, g);
-  else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16>), grid, block, 0, st, g);
+  if (g.packed) {
+    if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4, true>), grid, block, 0, st, g);
+    else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8, true>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16, true>), grid, block, 0, st, g);
+  } else {
+    if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4, false>), grid, block, 0, st, g);
+    else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8, false>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16, false>), grid, block, 0, st, g);
+  }
 }
 
-int gemm_launch_splits(int epi, int N, int K) { return epi == EPI_ARGMAX ? 1 : gemm_splits(N, K); }
+// The fused epilogues (argmax, GELU) need the whole K sum in one workgroup.
+int gemm_launch_splits(int epi, int N, int K) {
+  return (epi == EPI_ARGMAX || epi == EPI_GELU) ? 1 : gemm_splits(N, K);
+}
 
 void launch_gemm_mfma(int epi, GemmArgs g, hipStream_t st) {
   g.ntiles = (g.N + kNT - 1) / kNT;
   g.KB = g.K / 32;
   g.S = gemm_launch_splits(epi, g.N, g.K);
   if (epi == EPI_ARGMAX) launch_one<EPI_ARGMAX>(g, st);
+  else if (epi == EPI_GELU) launch_one<EPI_GELU>(g, st);
   else launch_one<EPI_PARTIAL>(g, st);
 }
 
-void launch_gelu_reduce(GemmArgs g, hipStream_t st) {
-  g.S = gemm_splits(g.N, g.K);
-  const size_t total4 = (size_t)g.M * g.N / 4;
-  const dim3 grid((unsigned)std::min<size_t>((total4 + 255) / 256, 4096)), block(256);
-  hipLaunchKernelGGL(gelu_reduce_kernel, grid, block, 0, st, g);
-}
 
 void launch_argmax_final(int M, int nrec, const void* part, const RowDesc* rows, int* greedy,
                          float* margin, int* err, hipStream_t st) {

@@ -35,13 +35,15 @@ class Session:
     def __init__(self, cfg: Config, params, batch: int, k_max: int, frames, *,
                  layout: int = ad.AD_PADDED, packed_encoder: bool = False,
                  page_seed: int | None = 0, want_logits: bool = False, device: str = "cuda",
-                 extra_pages: int = 0):
+                 extra_pages: int = 0, pack_weights: bool = True):
         self.cfg, self.B, self.k_max, self.layout = cfg, batch, k_max, layout
         self.device = device
         self.dt = torch_dtype(cfg)
         L, d, H = cfg.n_layers, cfg.d_model, cfg.n_heads
         self.params = params if isinstance(params, list) else upload_params(cfg, params, device)
         self.model = ad.Model(cfg, self.params)
+        if pack_weights and cfg.dtype == "bf16":   # tiled weights for the matrix-core GEMMs
+            self.model.pack(torch.empty(self.model.pack_size(), dtype=torch.uint8, device=device))
         i32 = dict(dtype=torch.int32, device=device)
 
         # paged self-KV: every sequence may reach the last position

@@ -46,6 +46,12 @@ def test_param_count_and_model_validation(ad):
     bad = ad.model_desc(cfg.with_(d_model=100))
     assert ad.LIB.ad_model_create(ctypes.byref(bad), fake, 44, ctypes.byref(h)) == -5
     assert b"64 * n_heads" in ad.LIB.ad_last_error()
+    f32 = ad.model_desc(cfg.with_(dtype="f32"))
+    h32 = ctypes.c_void_p()
+    assert ad.LIB.ad_model_create(ctypes.byref(f32), fake, 44, ctypes.byref(h32)) == 0
+    n32 = ctypes.c_size_t()
+    assert ad.LIB.ad_model_pack_size(h32, ctypes.byref(n32)) == -5
+    ad.LIB.ad_model_destroy(h32)
     bad = ad.model_desc(cfg.with_(vocab=0))
     assert ad.LIB.ad_model_create(ctypes.byref(bad), fake, 44, ctypes.byref(h)) == -2
     desc.dtype = 7
@@ -59,6 +65,13 @@ def test_param_count_and_model_validation(ad):
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), nulls, 44, ctypes.byref(h)) == -1
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
     n = ctypes.c_size_t()
+    assert ad.LIB.ad_model_pack_size(h, ctypes.byref(n)) == 0
+    # per layer 6 tiled matrices, then the LM head: N rounded up to 128 columns
+    want = 2 * (2 * (384 * 128 + 128 * 128 * 3 + 256 * 128 + 128 * 256) + 128 * 128)
+    assert n.value == want
+    assert ad.LIB.ad_model_pack(h, 0x1008, n.value, None) == -1      # misaligned
+    assert ad.LIB.ad_model_pack(h, 0x1000, n.value - 1, None) == -3  # too small
+    assert ad.LIB.ad_model_pack(h, None, 0, None) == 0               # back to row-major
     assert ad.LIB.ad_workspace_size(h, 8, 2, 3, ctypes.byref(n)) == 0 and n.value > 0
     assert ad.LIB.ad_workspace_size(h, 0, 2, 3, ctypes.byref(n)) == -2
     assert ad.LIB.ad_workspace_size(h, 8, 2, -1, ctypes.byref(n)) == -2

@@ -177,3 +177,18 @@ def test_block_ending_at_last_position():
     st = oracle_state(cfg, model, b, n, int(wl.T[b]), int(wl.t0[b]))
     ref = od.verify(model, st, blocks[b][1:])
     compare_sequence(cfg, sess, res, b, blocks[b], ref, n)
+
+
+def test_tiled_weights_are_bit_identical():
+    """ad_model_pack only changes where the GEMMs read their weights from."""
+    cfg, params, wl = _setup("bf16")
+    blocks = [np.concatenate([[wl.t0[b]], wl.fill_any[b]]).astype(np.int64) for b in range(wl.batch)]
+    out = []
+    for pack in (True, False):
+        sess = device_session(cfg, params, wl, want_logits=True)
+        if not pack:
+            sess.model.pack(None)
+        sess.step(blocks)
+        out.append(sess.results())
+    for key in ("accept_len", "out_tokens", "greedy", "logits", "hidden"):
+        np.testing.assert_array_equal(out[0][key], out[1][key])
