@@ -140,14 +140,16 @@ typedef struct {
  * Encoder keys/values (the decoder's view of the frozen audio encoding, computed once
  * per utterance by ad_cross_kv_prefill).  data holds
  *   n_layers * 2 * n_heads * frames_cap * 64 elements of the model dtype
- * arranged as [layer][K|V][head][frame slot], frames in 16-frame tiles (private order).
+ * arranged as [layer][head][32-frame block][K|V] (private order within a block: the
+ * operand order of the attention products).
  * Sequence b uses slots enc_off[b] .. enc_off[b] + enc_len[b] - 1; enc_off[b] must be
- * a multiple of 16.  PADDED encoders use enc_off[b] = b * T_max, PACKED ones a running
- * sum of T_b rounded up to 16; both give identical results.
+ * a multiple of 32 (AD_ERR_FRAMES otherwise).  PADDED encoders use enc_off[b] =
+ * b * T_max, PACKED ones a running sum of T_b rounded up to 32; both give identical
+ * results.
  */
 typedef struct {
   void* data;                 /* device                                              */
-  int32_t frames_cap;         /* multiple of 16                                      */
+  int32_t frames_cap;         /* multiple of 32                                      */
   const int32_t* enc_len;     /* device [B]: T_b                                     */
   const int32_t* enc_off;     /* device [B]                                          */
 } ad_cross;
@@ -186,7 +188,7 @@ ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max
  * (the decoder reuses the encoded audio at every step; paper, section 1 and appendix
  * "Draft architecture").  enc is device [frames_cap][d] of the model dtype, sequence b
  * at rows enc_off[b].. (rows outside any sequence are projected too and never read).
- * Errors: AD_EINVAL, AD_ERANGE (frames_cap not a positive multiple of 16).
+ * Errors: AD_EINVAL, AD_ERANGE (frames_cap not a positive multiple of 32).
  */
 ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross,
                               void* stream);

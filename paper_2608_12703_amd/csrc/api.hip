@@ -487,8 +487,8 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->layout == AD_PACKED && (s->rows < s->batch || s->rows > full))
     return fail(AD_ERANGE, "packed rows must lie in [batch, batch * (k_max + 1)]");
   if (s->kv.num_pages < 1 || s->kv.pages_per_seq < 1) return fail(AD_ERANGE, "empty page pool");
-  if (s->cross.frames_cap < ad::kTile || s->cross.frames_cap % ad::kTile)
-    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 16");
+  if (s->cross.frames_cap < ad::kCrossBlock || s->cross.frames_cap % ad::kCrossBlock)
+    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 32");
   const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");
@@ -510,8 +510,8 @@ ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch
 
 ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross, void* stream) {
   if (!model || !enc || !cross || !cross->data) return fail(AD_EINVAL, "NULL argument");
-  if (cross->frames_cap < ad::kTile || cross->frames_cap % ad::kTile)
-    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 16");
+  if (cross->frames_cap < ad::kCrossBlock || cross->frames_cap % ad::kCrossBlock)
+    return fail(AD_ERANGE, "frames_cap must be a positive multiple of 32");
   const ad_model_desc& D = model->desc;
   (void)hipGetLastError();
   hipStream_t st = (hipStream_t)stream;

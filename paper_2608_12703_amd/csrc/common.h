@@ -87,24 +87,41 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 }
 
 // ----------------------------------------------------------------- cache layouts
-// Self-KV pool: [layer][K|V][page][head][tile]; cross-KV: [layer][K|V][head][frame tile].
-// A 16-token x 64-lane tile holds keys token-major (t * 64 + j: a token's 64 lanes are
-// one 128-byte line) and values lane-major (j * 16 + t: the 16 tokens of one lane are
-// contiguous, the order the value operand of the P.V product is read in).
+// Self-KV pool: [layer][K|V][page][head][tile]; a 16-token x 64-lane tile holds keys
+// token-major (t * 64 + j: a token's 64 lanes are one 128-byte line) and values
+// lane-major (j * 16 + t: the 16 tokens of one lane are contiguous).
+// Cross-KV: [layer][head][32-frame block][K|V], 2048 elements each for the keys and the
+// values of a block, in the operand order of the attention products (see cross_off): a
+// wave streams one contiguous range per key chunk and every load reads 1 KB contiguous.
+
+constexpr int kCrossBlock = 32;                        // frames per cross-K/V block
+constexpr int kCrossBlockElems = kCrossBlock * kHead;  // 2048
 
 __device__ __forceinline__ size_t kv_tile_base(int layer, int kv, int page, int head,
                                                int num_pages, int H) {
   return ((((size_t)layer * 2 + kv) * num_pages + page) * H + head) * (size_t)kTileElems;
 }
-__device__ __forceinline__ size_t cross_base(int layer, int kv, int head, int H, int frames_cap) {
-  return (((size_t)layer * 2 + kv) * H + head) * (size_t)frames_cap * kHead;
+// start of one layer's, one head's cross K/V (keys and values of frames_cap frames)
+__device__ __forceinline__ size_t cross_base(int layer, int head, int H, int frames_cap) {
+  return ((size_t)layer * H + head) * (size_t)frames_cap * kHead * 2;
 }
 __device__ __forceinline__ int tile_off(int kv, int t, int j) {
   return kv == 0 ? t * kHead + j : j * kTile + t;
 }
-// element (frame f, lane j) of one head's cross K (kv = 0) or V (kv = 1)
+// Element (frame f, lane j) of one head's cross K (kv = 0) or V (kv = 1).  Within a
+// 32-frame block the score product takes its 16 key rows in two passes tt, row c16
+// holding frame 8 (c16 / 4) + 4 tt + c16 % 4, lane group g supplying lanes
+// 16 g .. 16 g + 15 in two 8-lane halves: keys sit at (tt, half, g * 16 + c16, 8 lanes).
+// The value product takes, per 16-lane tile dt, lane dt * 16 + c16 and frames
+// 8 g .. 8 g + 7: values sit at (dt, g * 16 + c16, 8 frames).
 __device__ __forceinline__ size_t cross_off(int kv, int f, int j) {
-  return (size_t)(f / kTile) * kTileElems + tile_off(kv, f % kTile, j);
+  const size_t o = ((size_t)(f / kCrossBlock) * 2 + kv) * kCrossBlockElems;
+  const int t = f % kCrossBlock;
+  if (kv == 0) {
+    const int c16 = 4 * (t / 8) + (t & 3), tt = (t / 4) & 1;
+    return o + ((tt * 2 + ((j / 8) & 1)) * 64 + (j / 16) * 16 + c16) * 8 + (j & 7);
+  }
+  return o + ((j / 16) * 64 + (t / 8) * 16 + (j & 15)) * 8 + (t & 7);
 }
 
 // ----------------------------------------------------------------- MFMA operands

@@ -66,21 +66,31 @@ template <bool CROSS>
 __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, int h, int blk,
                                            int k_beg, int k_end, int pg_lane, int c16, int grp,
                                            KVTiles& t) {
+  if (CROSS) {
+    // one 32-frame block: keys and values already in operand order, 1 KB per load
+    const int b0 = blk < k_end ? blk : k_beg + (k_end - 1 - k_beg) / kCrossBlock * kCrossBlock;
+    const size_t bo = (size_t)((s.enc_off + b0) / kCrossBlock) * 2 * kCrossBlockElems + (grp * 16 + c16) * 8;
+    const uint16_t* kp = a.kv + cross_base(a.layer, h, a.H, a.frames_cap) + bo;
+    const uint16_t* vp = kp + kCrossBlockElems;
+    t.k00 = *(const uint4*)(kp + 0 * 512);
+    t.k01 = *(const uint4*)(kp + 1 * 512);
+    t.k10 = *(const uint4*)(kp + 2 * 512);
+    t.k11 = *(const uint4*)(kp + 3 * 512);
+    t.v0 = *(const uint4*)(vp + 0 * 512);
+    t.v1 = *(const uint4*)(vp + 1 * 512);
+    t.v2 = *(const uint4*)(vp + 2 * 512);
+    t.v3 = *(const uint4*)(vp + 3 * 512);
+    return;
+  }
   const uint16_t* kb[2];
   const uint16_t* vb[2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     int t0 = blk + 16 * u;
     t0 = t0 < k_end ? t0 : k_beg + (k_end - 1 - k_beg) / kTile * kTile;
-    if (CROSS) {
-      const size_t tile = (size_t)((s.enc_off + t0) / kTile) * kTileElems;
-      kb[u] = a.kv + cross_base(a.layer, 0, h, a.H, a.frames_cap) + tile;
-      vb[u] = a.kv + cross_base(a.layer, 1, h, a.H, a.frames_cap) + tile;
-    } else {
-      const int pg = __shfl(pg_lane, (t0 - k_beg) / kTile, kWave);
-      kb[u] = a.kv + kv_tile_base(a.layer, 0, pg, h, a.num_pages, a.H);
-      vb[u] = a.kv + kv_tile_base(a.layer, 1, pg, h, a.num_pages, a.H);
-    }
+    const int pg = __shfl(pg_lane, (t0 - k_beg) / kTile, kWave);
+    kb[u] = a.kv + kv_tile_base(a.layer, 0, pg, h, a.num_pages, a.H);
+    vb[u] = a.kv + kv_tile_base(a.layer, 1, pg, h, a.num_pages, a.H);
   }
   // key rows: lane c16 of product tt reads key 8 (c16 / 4) + 4 tt + c16 % 4, i.e. tile
   // c16 / 8, token 8 ((c16 / 4) % 2) + 4 tt + c16 % 4; lane group grp reads dims

@@ -21,7 +21,7 @@ __global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
       const int r1 = a.cu_rows[b + 1];
       if (row0 < 0 || r1 > a.rows || r1 - row0 != kb + 1) e |= 1;
     }
-    if (T < 1 || T > a.max_frames || off < 0 || (off & (kTile - 1)) || off + T > a.frames_cap)
+    if (T < 1 || T > a.max_frames || off < 0 || (off % kCrossBlock) || off + T > a.frames_cap)
       e |= 8;
     if (!(e & 1)) {
       const int last_page = (n + kb) / kTile;

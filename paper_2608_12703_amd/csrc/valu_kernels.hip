@@ -69,7 +69,7 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
       }
     } else if (EPI == EPI_XKV) {
       const int kv = n / e.d, h = (n % e.d) / kHead, j = n % kHead;
-      S::st((typename S::T*)e.cache, cross_base(e.layer, kv, h, e.H, e.frames_cap) + cross_off(kv, m, j), v);
+      S::st((typename S::T*)e.cache, cross_base(e.layer, h, e.H, e.frames_cap) + cross_off(kv, m, j), v);
     }
   }
 }
@@ -142,8 +142,8 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
         if (t < n_keys) {
           size_t bk, bv;
           if (CROSS) {
-            bk = cross_base(layer, 0, h, H, frames_cap) + cross_off(0, s.enc_off + t, j);
-            bv = cross_base(layer, 1, h, H, frames_cap) + cross_off(1, s.enc_off + t, j);
+            bk = cross_base(layer, h, H, frames_cap) + cross_off(0, s.enc_off + t, j);
+            bv = cross_base(layer, h, H, frames_cap) + cross_off(1, s.enc_off + t, j);
           } else {
             int pg = block_table[(size_t)b * pages_per_seq + t / kTile];
             pg = min(max(pg, 0), num_pages - 1);

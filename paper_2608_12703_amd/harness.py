@@ -13,8 +13,9 @@ from . import ad, synth
 from .configs import MAX_FRAMES, MAX_POS, PAGE, Config
 
 
-def _ceil16(x: int) -> int:
-    return (x + PAGE - 1) // PAGE * PAGE
+def _ceil32(x: int) -> int:
+    """Encoder slots are allotted in 32-frame blocks."""
+    return (x + 31) // 32 * 32
 
 
 def torch_dtype(cfg: Config):
@@ -62,9 +63,9 @@ class Session:
         assert len(frames) == batch and all(1 <= t <= MAX_FRAMES for t in frames)
         self.frames = frames
         if packed_encoder:
-            off = np.concatenate([[0], np.cumsum([_ceil16(t) for t in frames])])
+            off = np.concatenate([[0], np.cumsum([_ceil32(t) for t in frames])])
         else:
-            tmax = _ceil16(max(frames))
+            tmax = _ceil32(max(frames))
             off = np.arange(batch + 1) * tmax
         self.frames_cap = int(off[-1])
         self.enc_off = torch.tensor(off[:-1], **i32)
