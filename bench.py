@@ -14,7 +14,7 @@ update is undone by a 128-byte device copy after the step) so every step does th
 work.  value = emitted tokens per step (accepted drafts + the bonus token, summed over
 the batch) / step time.
 
-Prints one JSON line (rank 0, N = 1 only: this build runs on one GPU).
+Prints one JSON line (N = 1 only: the step is measured on one GPU).
 """
 from __future__ import annotations
 
@@ -113,8 +113,9 @@ def cpu_baseline(cfg, params, wl, b=0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs the verify step on one GPU; --gpus must be 1 "
-                                   "(data-parallel sharding over sequences is described in DESIGN.md)"}))
+        print(json.dumps({"error": "the verify step is measured on one GPU; --gpus must be 1 "
+                                   "(sequences are independent: several GPUs would each run their "
+                                   "own sequences with a weight replica and no exchange)"}))
         sys.exit(2)
     import torch
 
