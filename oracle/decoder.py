@@ -66,6 +66,17 @@ def attention(q, K, V, visible):
     return out
 
 
+def attention_probs(q, K, visible):
+    """Attention weights of a few query rows, per head: [r, H, n_keys], the softmax of
+    q.k / 8 over keys 0..visible[i]-1 (zero past them)."""
+    P = np.zeros((q.shape[0], q.shape[1], K.shape[0]))
+    for i in range(q.shape[0]):
+        nv = int(visible[i])
+        s = np.einsum("hd,thd->ht", q[i], K[:nv]) / np.sqrt(HEAD)
+        P[i, :, :nv] = softmax(s)
+    return P
+
+
 # ---------------------------------------------------------------------- model / state
 
 class Model:
@@ -135,10 +146,12 @@ class BlockOut:
     logits: np.ndarray      # [r, V] float64
     hidden: np.ndarray      # [r, d] final-LN output
     new_kv: list            # per layer (K, V) of the block rows, [r, H, 64], stored
+    xattn: np.ndarray | None = None   # [r, H, T] cross-attention weights at the probed layer
 
 
-def forward_block(model: Model, state: SeqState, tokens) -> BlockOut:
-    """One causal decoder pass over ``tokens`` placed at positions n..n+r-1."""
+def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None = None) -> BlockOut:
+    """One causal decoder pass over ``tokens`` placed at positions n..n+r-1.  With
+    ``probe_layer`` set, also returns that layer's cross-attention weights."""
     tokens = np.asarray(tokens, dtype=np.int64)
     r, n, d, H = len(tokens), state.n, model.d, model.H
     if n + r > MAX_POS:
@@ -146,6 +159,7 @@ def forward_block(model: Model, state: SeqState, tokens) -> BlockOut:
     pos = n + np.arange(r)
     x = model.w("tok_emb")[tokens] + model.w("pos_emb")[pos]
     new_kv = []
+    xattn = None
     for layer in range(model.L):
         h = layer_norm(x, model.lw(layer, "ln1_g"), model.lw(layer, "ln1_b"))
         qkv = h @ model.lw(layer, "w_qkv").T + model.lw(layer, "b_qkv")
@@ -161,6 +175,8 @@ def forward_block(model: Model, state: SeqState, tokens) -> BlockOut:
         q = (h @ model.lw(layer, "w_xq").T + model.lw(layer, "b_xq")).reshape(r, H, HEAD)
         Kx, Vx = state.cross[layer]
         a = attention(q, Kx, Vx, visible=np.full(r, Kx.shape[0])).reshape(r, d)
+        if layer == probe_layer:
+            xattn = attention_probs(q, Kx, visible=np.full(r, Kx.shape[0]))
         x = x + a @ model.lw(layer, "w_xo").T + model.lw(layer, "b_xo")
 
         h = layer_norm(x, model.lw(layer, "ln3_g"), model.lw(layer, "ln3_b"))
@@ -169,7 +185,7 @@ def forward_block(model: Model, state: SeqState, tokens) -> BlockOut:
         new_kv.append((k, v))
     hidden = layer_norm(x, model.w("lnf_g"), model.w("lnf_b"))
     logits = hidden @ model.w("tok_emb").T
-    return BlockOut(logits, hidden, new_kv)
+    return BlockOut(logits, hidden, new_kv, xattn)
 
 
 # ---------------------------------------------------------------------- verify / AR
@@ -251,3 +267,36 @@ def spec_decode_heads(model: Model, state: SeqState, heads_w, n_tokens: int):
         toks += r.emitted
         hidden, state = r.hidden[r.accepted], r.state
     return toks[:n_tokens], accepts, rounds
+
+
+# ---------------------------------------------------------------------- anchor readout
+
+@dataclass
+class Anchor:
+    frame: int            # argmax over frames of the head-averaged weights (lowest index)
+    peak: float           # the head-averaged weight there
+    margin: float         # its top-1 minus top-2 over frames
+    mean: np.ndarray      # [T] head-averaged weights of the row
+
+
+def anchor_of(xattn_row: np.ndarray) -> Anchor:
+    """Audio position from the target's verification attention (paper, section "Correction
+    and Cost", paragraph "Verification-Attention Correction"; appendix "Runtime
+    Correction"): average one query row's cross-attention weights over the heads at the
+    selected layer and take the peak frame.  xattn_row: [H, T]."""
+    mean = np.asarray(xattn_row, np.float64).mean(axis=0)
+    t = argmax_lowest(mean)
+    return Anchor(t, float(mean[t]), top2_margin(mean) if mean.size > 1 else float("inf"), mean)
+
+
+def verify_with_anchor(model: Model, state: SeqState, drafts, layer: int):
+    """verify() plus the anchor read from the cross-attention at ``layer`` of block row a,
+    the last verified position (its output is the bonus token, so its audio attention
+    marks where the next draft should start)."""
+    drafts = [int(t) for t in drafts]
+    out = forward_block(model, state, [state.t0] + drafts, probe_layer=layer)
+    greedy, margins = decide(out.logits)
+    a = accept_length(drafts, greedy)
+    res = VerifyOut(greedy, a, emitted_tokens(greedy, a), margins, out.logits, out.hidden,
+                    commit(state, out, a, greedy[a]), out.new_kv)
+    return res, anchor_of(out.xattn[a])
