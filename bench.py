@@ -44,6 +44,9 @@ def parse():
     p.add_argument("--layout", default="padded", choices=["padded", "packed"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-kernel-profile", action="store_true")
+    p.add_argument("--anchor-layer", type=int, default=-2,
+                   help="also time the step with the verification-attention anchor readout at "
+                        "this layer (-2: three quarters of the depth; -1: skip)")
     p.add_argument("--copy-calibration-mb", type=int, default=0,
                    help="after the timed steps, copy a buffer of this many MiB once (a plain "
                         "copy of known size that calibrates HBM byte counters)")
@@ -201,6 +204,39 @@ def main():
                 "launch_us": round(per_launch_s * 1e6, 2), "launches_timed": n_launch}
         log(f"cross-attention: {per_launch_s * 1e6:.1f} us/launch, {achieved:.0f} GB/s")
 
+    anchor = None
+    if args.anchor_layer != -1:
+        # The same steps with the anchor readout after the accept scan: its two kernels
+        # timed with an event pair, and the step-time difference.
+        layer = 3 * cfg.n_layers // 4 if args.anchor_layer < -1 else args.anchor_layer
+        sess.anchor_layer = layer
+        sess.prepare(blocks)
+        for _ in range(args.warmup):
+            one_step()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            one_step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms_a = ev0.elapsed_time(ev1) / args.steps
+        ad.profile_enable(sess.model, ad.PROF_ANCHOR, args.steps)
+        for _ in range(args.steps):
+            one_step()
+        tot, n_launch = ad.profile_read(sess.model)
+        ad.profile_enable(sess.model, ad.PROF_ANCHOR, 0)
+        ra = sess.results()
+        assert np.array_equal(ra["accept_len"], res["accept_len"]) and np.all(ra["anchor"] >= 0)
+        key_bytes = int(np.sum(wl.T)) * cfg.d_model * roofline.elem_bytes(cfg)
+        us = tot / n_launch * 1e3
+        anchor = {"layer": layer, "us_per_step_events": round(us, 2),
+                  "us_per_step_delta": round((ms_a - ms) * 1e3, 2), "key_bytes": key_bytes,
+                  "achieved_GBps": round(key_bytes / (us * 1e-6) / 1e9, 1)}
+        log(f"anchor readout at layer {layer}: {us:.1f} us/step (events), "
+            f"{(ms_a - ms) * 1e3:.1f} us/step (step difference)")
+        sess.anchor_layer = -1
+        sess.prepare(blocks)
+
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
@@ -232,6 +268,7 @@ def main():
         "step_hbm_frac": round(sb["total"] / (ms / 1e3) / roofline.HBM_PEAK, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "anchor_readout": anchor,
     }
     print(json.dumps(out), flush=True)
 

@@ -174,6 +174,17 @@ typedef struct {
   int32_t* err_flag;          /* device [1]: AD_ERR_* bits are OR-ed in              */
   void* workspace;            /* device scratch, >= ad_workspace_size() bytes        */
   size_t workspace_bytes;
+  /* Verification-attention anchor readout (optional; paper, section "Correction and
+   * Cost", paragraph "Verification-Attention Correction", and appendix "Runtime
+   * Correction"): with 0 <= anchor_layer < n_layers, after the accept scan the
+   * cross-attention weights of block row a_b (the last verified position) at that layer
+   * are recomputed from the layer's queries and key cache, averaged over the heads, and
+   * out_anchor[b] receives the frame 0 .. T_b - 1 with the largest average (lowest index
+   * on ties; -1 for a skipped sequence), out_anchor_peak[b] (optional) that average.
+   * anchor_layer = -1 turns the readout off (out_anchor may then be NULL).           */
+  int32_t anchor_layer;
+  int32_t* out_anchor;        /* device [B] out                                      */
+  float* out_anchor_peak;     /* device [B] out (optional)                           */
 } ad_step;
 
 /* Bytes of workspace a step with up to max_rows rows, max_batch sequences and draft
@@ -268,6 +279,7 @@ ad_status ad_kv_export(const ad_model* model, const ad_kv* kv, int32_t b, void* 
 #define AD_PROF_LM_HEAD 4     /* LM head with the fused argmax                     */
 #define AD_PROF_XQ_CROSS 5    /* cross-attention query projection + cross-attention */
 #define AD_PROF_XQ 6          /* cross-attention query projection alone             */
+#define AD_PROF_ANCHOR 7      /* the anchor readout's two kernels (bf16 models)     */
 ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches);
 ad_status ad_profile_read(ad_model* model, double* total_ms, int32_t* launches);
 

@@ -44,7 +44,8 @@ class Step(ctypes.Structure):
                 ("tokens", _ptr), ("k", _ptr), ("cu_rows", _ptr), ("kv", KV), ("cross", Cross),
                 ("accept_len", _ptr), ("out_tokens", _ptr), ("out_greedy", _ptr),
                 ("out_logits", _ptr), ("out_hidden", _ptr), ("out_margin", _ptr),
-                ("err_flag", _ptr), ("workspace", _ptr), ("workspace_bytes", _size)]
+                ("err_flag", _ptr), ("workspace", _ptr), ("workspace_bytes", _size),
+                ("anchor_layer", _i32), ("out_anchor", _ptr), ("out_anchor_peak", _ptr)]
 
 
 def _load():
@@ -83,7 +84,7 @@ EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model
            "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_profile_enable", "ad_profile_read")
-PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD, PROF_XQ_CROSS, PROF_XQ = 1, 2, 3, 4, 5, 6
+PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD, PROF_XQ_CROSS, PROF_XQ, PROF_ANCHOR = 1, 2, 3, 4, 5, 6, 7
 
 
 class ADError(RuntimeError):

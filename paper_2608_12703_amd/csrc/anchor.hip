@@ -1,0 +1,188 @@
+// Verification-attention anchor readout (paper, section "Correction and Cost", paragraph
+// "Verification-Attention Correction"; appendix "Runtime Correction"): the target's
+// audio attention during verification, averaged over the heads of one decoder layer,
+// peaks at the audio position of the next token, which centres the next draft window.
+// Like the paper's runtime source, it is recomputed after verification from the layer's
+// queries (kept by the cross-attention kernel of that layer) and its existing key cache;
+// no extra decoder pass.  The row read is block row a_b, the last verified position,
+// whose output is the bonus token.
+//
+// Two kernels after the accept scan:
+//   scores: one workgroup per (head, sequence, 384-frame chunk) computes q.k / 8 for the
+//           chunk's frames (float32) plus the chunk's (max, sum of exp(s - max));
+//   pick:   one workgroup per sequence combines the chunk statistics into each head's
+//           softmax normaliser (chunk order), averages the heads' weights per frame
+//           (head order) and takes the frame with the largest average (lowest index on
+//           ties).
+// Keys are read once (the layer's K of every sequence, as the attention kernel does for
+// one of its products); the scores round-trip through a small scratch buffer.
+#include "common.h"
+#include "launch.h"
+
+namespace ad {
+
+template <class S>
+__global__ void __launch_bounds__(256) anchor_scores_kernel(AnchorArgs a) {
+  constexpr int kBlocks = kAnchorChunk / kCrossBlock;   // 12
+  __shared__ float part[kBlocks][kCrossBlock][9];       // dot products of 8-dim pieces
+  __shared__ float red[4];
+  const int h = blockIdx.x, b = blockIdx.y, c = blockIdx.z;
+  const SeqDesc s = a.seqs[b];
+  const int acc = a.accept_len[b];
+  if (!s.valid || acc < 0) return;
+  const int f0 = c * kAnchorChunk;
+  if (f0 >= s.T) return;
+  const int f1 = min(f0 + kAnchorChunk, s.T);
+  const int nblk = (f1 - f0 + kCrossBlock - 1) / kCrossBlock;
+  const int tid = threadIdx.x;
+  // this thread: frame t of every block of the chunk, dims j0 .. j0 + 7 (16 contiguous
+  // bytes of the key layout)
+  const int t = tid >> 3, g = tid & 7, j0 = g * 8;
+  const float* qp = a.q + (size_t)(s.row0 + acc) * a.d + h * kHead + j0;
+  const float4 qa = *(const float4*)qp, qb = *(const float4*)(qp + 4);
+  const float q[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+  const typename S::T* kb = (const typename S::T*)a.kv + cross_base(a.layer, h, a.H, a.frames_cap);
+  // every block's piece requested before any is used (blocks past the chunk reload its
+  // last block; frames past T read valid slots of the sequence's 32-frame block)
+  float kv[kBlocks][8];
+#pragma unroll
+  for (int i = 0; i < kBlocks; ++i) {
+    const int bi = i < nblk ? i : nblk - 1;
+    const typename S::T* p = kb + cross_off(0, s.enc_off + f0 + bi * kCrossBlock + t, j0);
+    if constexpr (sizeof(typename S::T) == 2) {   // 8 bf16 keys: one 16-byte load
+      const uint4 v = *(const uint4*)p;
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        kv[i][2 * e] = bf16_to_f32(w[e] & 0xffff);
+        kv[i][2 * e + 1] = bf16_to_f32(w[e] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kv[i][e] = S::ld(p, e);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kBlocks; ++i) {
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dot = fmaf(q[e], kv[i][e], dot);
+    part[i][t][g] = dot;
+  }
+  __syncthreads();
+  // frame scores (pieces summed in dim order; two frames per thread cover the chunk's
+  // 384), then the chunk's max and sum
+  float* sc = a.score + ((size_t)b * a.H + h) * a.max_frames;
+  float sv[2];
+  float m = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = tid + u * 256, i = idx / kCrossBlock, tt = idx % kCrossBlock;
+    const int f = f0 + idx;
+    sv[u] = -INFINITY;
+    if (i < nblk && f < f1) {
+      float d = 0.f;
+#pragma unroll
+      for (int gg = 0; gg < 8; ++gg) d += part[i][tt][gg];
+      sv[u] = d * 0.125f;
+      sc[f] = sv[u];
+    }
+    m = fmaxf(m, sv[u]);
+  }
+  m = wave_max(m);
+  if ((tid & 63) == 0) red[tid >> 6] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float e = 0.f;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    if (sv[u] != -INFINITY) e += expf(sv[u] - m);
+  const float l = block_sum<4>(e, red);
+  if (tid == 0) a.stats[((size_t)b * a.H + h) * a.nchunks + c] = make_float2(m, l);
+}
+
+__global__ void __launch_bounds__(256) anchor_pick_kernel(AnchorArgs a) {
+  __shared__ float Mh[64], Lh[64];
+  __shared__ float bv[4];
+  __shared__ int bi[4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const SeqDesc s = a.seqs[b];
+  const int acc = a.accept_len[b];
+  if (!s.valid || acc < 0) {
+    if (tid == 0) {
+      a.out_anchor[b] = -1;
+      if (a.out_peak) a.out_peak[b] = 0.f;
+    }
+    return;
+  }
+  const int T = s.T, nch = (T + kAnchorChunk - 1) / kAnchorChunk;
+  // each head's softmax normaliser from its chunks, in chunk order
+  for (int h = tid; h < a.H; h += blockDim.x) {
+    const float2* st = a.stats + ((size_t)b * a.H + h) * a.nchunks;
+    float M = -INFINITY;
+    for (int c = 0; c < nch; ++c) M = fmaxf(M, st[c].x);
+    float L = 0.f;
+    for (int c = 0; c < nch; ++c) L += st[c].y * expf(st[c].x - M);
+    Mh[h] = M;
+    Lh[h] = L;
+  }
+  __syncthreads();
+  // head-averaged weight per frame; this thread's best (frames rise, so '>' keeps the
+  // lowest index among equal values)
+  const float* sc = a.score + (size_t)b * a.H * a.max_frames;
+  float best = -1.f;
+  int best_t = 0x7fffffff;
+  for (int t = tid; t < T; t += blockDim.x) {
+    float w = 0.f;
+    for (int h = 0; h < a.H; ++h) w += expf(sc[(size_t)h * a.max_frames + t] - Mh[h]) / Lh[h];
+    w = w / (float)a.H;
+    if (w > best) {
+      best = w;
+      best_t = t;
+    }
+  }
+  // block argmax: larger value, then lower frame
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ov = __shfl_xor(best, o, kWave);
+    const int ot = __shfl_xor(best_t, o, kWave);
+    const bool take = (ov > best) | ((ov == best) & (ot < best_t));
+    best = take ? ov : best;
+    best_t = take ? ot : best_t;
+  }
+  if ((tid & 63) == 0) {
+    bv[tid >> 6] = best;
+    bi[tid >> 6] = best_t;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float v = bv[0];
+    int t = bi[0];
+    for (int w = 1; w < 4; ++w)
+      if ((bv[w] > v) | ((bv[w] == v) & (bi[w] < t))) {
+        v = bv[w];
+        t = bi[w];
+      }
+    a.out_anchor[b] = t;
+    if (a.out_peak) a.out_peak[b] = v;
+  }
+}
+
+size_t anchor_score_floats(int B, int H, int max_frames) {
+  return ((size_t)B * H * max_frames + 63) / 64 * 64;   // the statistics follow, aligned
+}
+
+size_t anchor_scratch_floats(int B, int H, int max_frames) {
+  const int nch = (max_frames + kAnchorChunk - 1) / kAnchorChunk;
+  return anchor_score_floats(B, H, max_frames) + 2 * (size_t)B * H * nch;
+}
+
+template <class S>
+void launch_anchor(const AnchorArgs& a, int B, hipStream_t st) {
+  hipLaunchKernelGGL(anchor_scores_kernel<S>, dim3(a.H, B, a.nchunks), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(anchor_pick_kernel, dim3(B), dim3(256), 0, st, a);
+}
+template void launch_anchor<F32>(const AnchorArgs&, int, hipStream_t);
+template void launch_anchor<BF16>(const AnchorArgs&, int, hipStream_t);
+
+}  // namespace ad

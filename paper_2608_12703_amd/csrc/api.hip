@@ -85,6 +85,8 @@ struct Workspace {
   uint16_t* hfrag; // bf16 path: F-wide product operand (GELU output)
   float* gpart;    // bf16 path: split-K partial products
   void* ampart;    // bf16 path: LM-head top-2 records
+  float* q_anchor; // the anchor layer's cross-attention queries [M][d]
+  float* xscore;   // anchor readout scratch (scores, then per-chunk statistics)
   int RT, qgroups;
   size_t bytes;
 };
@@ -108,6 +110,8 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
   w.q = (float*)take(4 * M * D);
   w.hidden = (float*)take(4 * M * D);
   w.greedy = (int*)take(4ull * M);
+  w.q_anchor = (float*)take(4 * M * D);
+  w.xscore = (float*)take(4 * ad::anchor_scratch_floats(B, d.n_heads, d.max_frames));
   if (d.dtype == AD_F32) {
     w.ln = (float*)take(4 * M * D);
     w.att = (float*)take(4 * M * D);
@@ -156,6 +160,26 @@ struct ProfScope {
   ~ProfScope() { stop(); }
 };
 
+ad::AnchorArgs anchor_args(const ad_model* m, const ad_step* s, const Workspace& w) {
+  const ad_model_desc& D = m->desc;
+  ad::AnchorArgs a{};
+  a.seqs = w.seqs;
+  a.accept_len = s->accept_len;
+  a.q = w.q_anchor;
+  a.kv = s->cross.data;
+  a.layer = s->anchor_layer;
+  a.H = D.n_heads;
+  a.d = D.d_model;
+  a.frames_cap = s->cross.frames_cap;
+  a.max_frames = D.max_frames;
+  a.nchunks = div_up(D.max_frames, ad::kAnchorChunk);
+  a.score = w.xscore;
+  a.stats = (float2*)(w.xscore + ad::anchor_score_floats(s->batch, D.n_heads, D.max_frames));
+  a.out_anchor = s->out_anchor;
+  a.out_peak = s->out_anchor_peak;
+  return a;
+}
+
 template <class S>
 void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipStream_t st) {
   const ad_model_desc& D = m->desc;
@@ -192,6 +216,8 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     ad::launch_layernorm<S>(M, d, w.x, lp(m, l, LN2_G), lp(m, l, LN2_B), w.ln, st);
     e.out = w.q; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_STORE, M, d, d, w.ln, lp(m, l, W_XQ), lp(m, l, B_XQ), e, st);
+    if (l == s->anchor_layer)
+      (void)hipMemcpyAsync(w.q_anchor, w.q, sizeof(float) * M * d, hipMemcpyDeviceToDevice, st);
     {
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
       ad::launch_cross_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->cross.data,
@@ -217,6 +243,7 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
   ad::launch_argmax(M, V, logits, V, w.rows, greedy, s->out_margin, s->err_flag, st);
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+  if (s->anchor_layer >= 0) ad::launch_anchor<S>(anchor_args(m, s, w), s->batch, st);
 }
 
 // bf16 model.  The projections write split-K partial products that the next kernel
@@ -287,6 +314,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     at.max_chunks = div_up(D.max_frames, ad::kCrossChunk);
     at.qkv_splits = ad::gemm_splits(d, d); at.qkv_n = d;
     at.qkv_bias = (const uint16_t*)lp(m, l, B_XQ);
+    at.q_save = l == s->anchor_layer ? w.q_anchor : nullptr;
     {
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
       ad::launch_attn_mfma(at, s->batch, st);
@@ -315,6 +343,10 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
   ad::launch_argmax_final(M, ad::lm_records(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
   ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+  if (s->anchor_layer >= 0) {
+    ProfScope ps(m, AD_PROF_ANCHOR, st);
+    ad::launch_anchor<ad::BF16>(anchor_args(m, s, w), s->batch, st);
+  }
 }
 
 ad_status validate_desc(const ad_model_desc* d) {
@@ -422,7 +454,7 @@ ad_status ad_model_destroy(ad_model* model) {
 ad_status ad_profile_enable(ad_model* model, int32_t kernel, int32_t max_launches) {
   if (!model) return fail(AD_EINVAL, "model is NULL");
   if (max_launches < 0 || max_launches > (1 << 20)) return fail(AD_ERANGE, "max_launches out of range");
-  if (max_launches > 0 && (kernel < AD_PROF_CROSS_ATTN || kernel > AD_PROF_XQ))
+  if (max_launches > 0 && (kernel < AD_PROF_CROSS_ATTN || kernel > AD_PROF_ANCHOR))
     return fail(AD_EINVAL, "unknown kernel class");
   prof_free(model);
   if (max_launches == 0) return AD_OK;
@@ -489,6 +521,10 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->kv.num_pages < 1 || s->kv.pages_per_seq < 1) return fail(AD_ERANGE, "empty page pool");
   if (s->cross.frames_cap < ad::kCrossBlock || s->cross.frames_cap % ad::kCrossBlock)
     return fail(AD_ERANGE, "frames_cap must be a positive multiple of 32");
+  if (s->anchor_layer < -1 || s->anchor_layer >= D.n_layers)
+    return fail(AD_ERANGE, "anchor_layer must be -1 or a layer index");
+  if (s->anchor_layer >= 0 && !s->out_anchor)
+    return fail(AD_EINVAL, "the anchor readout needs out_anchor");
   const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");

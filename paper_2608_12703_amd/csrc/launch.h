@@ -126,8 +126,29 @@ struct AttnArgs {
   const int* block_table;
   int pages_per_seq, frames_cap;
   int chunk, max_chunks, qgroups;   // max_chunks waves per workgroup (at most 8)
+  float* q_save;   // cross-attention only, may be NULL: the finished queries, [rows][d]
 };
 void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st);
+
+// Verification-attention anchor readout: for every valid sequence, block row a_b's
+// cross-attention weights at one layer (recomputed from the saved queries and the
+// layer's keys), averaged over heads; the frame with the largest average.
+constexpr int kAnchorChunk = 384;   // frames per workgroup of the score kernel
+struct AnchorArgs {
+  const SeqDesc* seqs;
+  const int* accept_len;
+  const float* q;          // [rows][d] finished queries of the layer
+  const void* kv;          // cross K/V cache
+  int layer, H, d, frames_cap, max_frames, nchunks;
+  float* score;            // scratch [B][H][max_frames]
+  float2* stats;           // scratch [B][H][nchunks]: (max, sum of exp(score - max))
+  int* out_anchor;         // [B]
+  float* out_peak;         // [B] or NULL
+};
+size_t anchor_score_floats(int B, int H, int max_frames);     // the scores' part
+size_t anchor_scratch_floats(int B, int H, int max_frames);   // scores + statistics
+template <class S>
+void launch_anchor(const AnchorArgs& a, int B, hipStream_t st);
 
 // LayerNorm of float32 rows into A-fragment order (hi/lo bf16) for the next product,
 // and optionally also as float32 rows (out may be NULL).

@@ -321,14 +321,17 @@ attn_mfma_kernel(AttnArgs a) {
 
   // finish the projection: this head's queries of the group, and (self-attention) the
   // keys / values of every block row of the sequence
+  // (the anchor readout keeps this layer's finished queries: q_save)
   {
     const float4 qv = finish(qp, qb, qe);
     if (threadIdx.x < 16 * 16) *(float4*)(qs + qr * kHead + qj) = q_on ? qv : float4{0.f, 0.f, 0.f, 0.f};
+    if (CROSS && a.q_save && q_on) *(float4*)(a.q_save + (size_t)(s.row0 + q0 + qr) * a.d + h * kHead + qj) = qv;
   }
   for (int idx = threadIdx.x + blockDim.x; idx < 16 * 16; idx += blockDim.x) {   // small blocks
     const int r = idx >> 4, j = (idx & 15) * 4;
-    *(float4*)(qs + r * kHead + j) =
-        r < nq ? finish_proj4(a, s.row0 + q0 + r, h * kHead + j) : float4{0.f, 0.f, 0.f, 0.f};
+    const float4 v = r < nq ? finish_proj4(a, s.row0 + q0 + r, h * kHead + j) : float4{0.f, 0.f, 0.f, 0.f};
+    *(float4*)(qs + r * kHead + j) = v;
+    if (CROSS && a.q_save && r < nq) *(float4*)(a.q_save + (size_t)(s.row0 + q0 + r) * a.d + h * kHead + j) = v;
   }
   if (!CROSS) {
     const float4 kv4 = finish(kp, kbias, ke);

@@ -82,6 +82,10 @@ class Session:
         self.out_logits = (torch.zeros(self.max_rows, cfg.vocab, dtype=torch.float32, device=device)
                            if want_logits else None)
         self.err_flag = torch.zeros(1, **i32)
+        # verification-attention anchor readout (anchor_layer -1: off)
+        self.anchor_layer = -1
+        self.out_anchor = torch.full((batch,), -1, **i32)
+        self.out_anchor_peak = torch.zeros(batch, dtype=torch.float32, device=device)
         self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch, k_max),
                                      dtype=torch.uint8, device=device)
         self.step_struct = None
@@ -147,7 +151,8 @@ class Session:
             ad.ptr(cu), self.kv_struct(), self.cross_struct(), self.accept_len.data_ptr(),
             self.out_tokens.data_ptr(), self.out_greedy.data_ptr(), ad.ptr(self.out_logits),
             self.out_hidden.data_ptr(), self.out_margin.data_ptr(), self.err_flag.data_ptr(),
-            self.workspace.data_ptr(), self.workspace.numel())
+            self.workspace.data_ptr(), self.workspace.numel(), int(self.anchor_layer),
+            self.out_anchor.data_ptr(), self.out_anchor_peak.data_ptr())
         self.cur_layout = layout
         return self.step_struct
 
@@ -180,4 +185,7 @@ class Session:
                "err": int(self.err_flag.item())}
         if self.out_logits is not None:
             out["logits"] = self.out_logits[: self.rows].cpu().numpy()
+        if self.anchor_layer >= 0:
+            out["anchor"] = self.out_anchor.cpu().numpy()
+            out["anchor_peak"] = self.out_anchor_peak.cpu().numpy()
         return out

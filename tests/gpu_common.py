@@ -133,3 +133,36 @@ def kv_close(gpu: np.ndarray, want: np.ndarray, what: str, dtype: str):
         floor = 1e-5 * rms
         bad = diff > np.abs(want) * 1e-5 + 1e-6 + floor
         assert not np.any(bad), f"{what}: {int(bad.sum())} cache values off by more than 1e-5"
+
+
+# Head-averaged attention weights: the GPU recomputes row a_b's scores in float32 from its
+# own queries, which carry the step's activation error.  A weight's relative error is
+# about its score's absolute error: scores of these models have a spread of ~0.5, and
+# the queries' relative error stays below 1e-3 (the logits of the 32-layer model differ
+# from the oracle's by ~1e-3 on an rms of 0.72), so |d score| <~ 5e-4.  Measured on the
+# small shapes: 6e-7 of the peak.  float32 models: the float32 accumulation spread.
+ANCHOR_REL = {"bf16": 5e-4, "f32": 1e-5}
+ANCHOR_STATS = []      # (seq, frame equal, |peak error| / peak, oracle margin / peak)
+
+
+def compare_anchor(cfg, res, b, ref: od.VerifyOut, anc: od.Anchor):
+    """Anchor readout of sequence b against the oracle's (when its accept decision is
+    comparable: the readout reads block row a_b).
+
+    The frame must equal the oracle's unless the oracle's top-2 gap is inside the error
+    bound; in every case the oracle's weight at the GPU's frame must lie within the bound
+    of the maximum, and the GPU's peak must match the oracle's weight at that frame."""
+    if int(res["accept_len"][b]) != ref.accepted:
+        return False
+    f, peak = int(res["anchor"][b]), float(res["anchor_peak"][b])
+    tol = ANCHOR_REL[cfg.dtype] * anc.peak
+    assert 0 <= f < anc.mean.size, f"seq {b}: anchor frame {f} outside 0..{anc.mean.size - 1}"
+    err = abs(peak - anc.mean[f])
+    ANCHOR_STATS.append((b, f == anc.frame, err / anc.peak, anc.margin / anc.peak))
+    print(f"  seq {b}: anchor gpu {f} oracle {anc.frame} (T {anc.mean.size}), peak {peak:.6e} "
+          f"vs {anc.mean[f]:.6e}, oracle margin {anc.margin / anc.peak:.2e} of peak")
+    assert err <= tol, f"seq {b}: anchor peak {peak} vs oracle {anc.mean[f]}"
+    assert anc.mean[f] >= anc.peak - 2 * tol, f"seq {b}: frame {f} is not a near-maximum"
+    if anc.margin > 2 * tol:
+        assert f == anc.frame, f"seq {b}: anchor frame {f} vs oracle {anc.frame}"
+    return True

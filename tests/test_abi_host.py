@@ -82,7 +82,7 @@ def _step(ad, **over):
     kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
     cross = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
     s = ad.Step(2, ad.AD_PADDED, 3, 8, 0x1000, 0x1000, None, kv, cross, 0x1000, 0x1000, None, None,
-                None, None, 0x1000, 0x1000, 1 << 40)
+                None, None, 0x1000, 0x1000, 1 << 40, -1, None, None)
     for k, v in over.items():
         setattr(s, k, v)
     return s
@@ -104,6 +104,9 @@ def test_verify_step_rejects_before_enqueue(ad):
     s = _step(ad)
     s.cross.frames_cap = 20
     assert run(s) == -2
+    assert run(_step(ad, anchor_layer=-2)) == -2
+    assert run(_step(ad, anchor_layer=cfg.n_layers)) == -2
+    assert run(_step(ad, anchor_layer=0)) == -1                     # readout without out_anchor
     assert run(_step(ad, workspace_bytes=100)) == -3
     assert b"workspace" in ad.LIB.ad_last_error()
     assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1

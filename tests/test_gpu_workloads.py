@@ -24,13 +24,14 @@ from paper_2608_12703_amd import ad, decode, synth
 from paper_2608_12703_amd.configs import CONFIGS, SOT_TOKEN
 from paper_2608_12703_amd.harness import Session, upload
 
-from gpu_common import MARGIN_EXCLUDE, compare_sequence, device_session, oracle_state
+from gpu_common import MARGIN_EXCLUDE, compare_anchor, compare_sequence, device_session, oracle_state
 
 pytestmark = pytest.mark.gpu
 
 
-def _sampled_step(cfg, sample, layout=ad.AD_PADDED):
-    """One verify step of the full batch; oracle-planted drafts for `sample`."""
+def _sampled_step(cfg, sample, layout=ad.AD_PADDED, anchor_layer=-1):
+    """One verify step of the full batch; oracle-planted drafts for `sample`.  With
+    anchor_layer set, the step also reads the verification-attention anchor there."""
     params = synth.make_params(cfg)
     wl = synth.make_step_workload(cfg)
     model = od.Model(cfg, params)
@@ -47,14 +48,20 @@ def _sampled_step(cfg, sample, layout=ad.AD_PADDED):
             d = wl.fill_any[b]
         blocks.append(np.concatenate([[wl.t0[b]], d]).astype(np.int64))
     sess = device_session(cfg, params, wl, layout=layout, packed_encoder=layout == ad.AD_PACKED)
+    sess.anchor_layer = anchor_layer
     sess.step(blocks)
     res = sess.results()
     assert res["err"] == 0
     for b in ids:
-        ref = od.verify(model, states[b], blocks[b][1:])
+        if anchor_layer >= 0:
+            ref, anc = od.verify_with_anchor(model, states[b], blocks[b][1:], anchor_layer)
+        else:
+            ref = od.verify(model, states[b], blocks[b][1:])
         print(f"[{cfg.name}] seq {b}: n={int(wl.n[b])} T={int(wl.T[b])} k={int(wl.k[b])} "
               f"accept gpu {int(res['accept_len'][b])} oracle {ref.accepted}")
         compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]))
+        if anchor_layer >= 0:
+            compare_anchor(cfg, res, b, ref, anc)
     return sess, res, blocks, wl
 
 
@@ -65,17 +72,23 @@ def test_small_bf16_sampled_sequences():
 
 def test_large_v3_bench_configuration_sampled_sequences():
     cfg = CONFIGS["large_v3_bf16"]
-    _sampled_step(cfg, lambda wl: [int(np.argmax(wl.n)), int(np.argmin(wl.n))])
+    # with the verification-attention anchor read at three quarters of the depth
+    _sampled_step(cfg, lambda wl: [int(np.argmax(wl.n)), int(np.argmin(wl.n))],
+                  anchor_layer=3 * cfg.n_layers // 4)
 
 
 def test_ragged_padded_and_packed_agree_and_match_oracle():
     cfg = CONFIGS["ragged_large_v3"]
     sample = lambda wl: [int(np.argmax(wl.k * 10000 + wl.T)), int(np.argmin(wl.T))]
-    sess, res, blocks, wl = _sampled_step(cfg, sample, layout=ad.AD_PADDED)
+    sess, res, blocks, wl = _sampled_step(cfg, sample, layout=ad.AD_PADDED,
+                                          anchor_layer=3 * cfg.n_layers // 4)
     # the same step in the packed row layout with packed encoder slots
     sess2 = device_session(cfg, sess.params, wl, layout=ad.AD_PACKED, packed_encoder=True)
+    sess2.anchor_layer = sess.anchor_layer
     sess2.step(blocks)
     res2 = sess2.results()
+    np.testing.assert_array_equal(res2["anchor"], res["anchor"])
+    np.testing.assert_array_equal(res2["anchor_peak"].view(np.uint32), res["anchor_peak"].view(np.uint32))
     np.testing.assert_array_equal(res2["accept_len"], res["accept_len"])
     np.testing.assert_array_equal(res2["out_tokens"], res["out_tokens"])
     rows = [sess.row_of(b, i) for b in range(wl.batch) for i in range(int(wl.k[b]) + 1)]
