@@ -101,10 +101,14 @@ __global__ void __launch_bounds__(256) anchor_scores_kernel(AnchorArgs a) {
   if (tid == 0) a.stats[((size_t)b * a.H + h) * a.nchunks + c] = make_float2(m, l);
 }
 
-__global__ void __launch_bounds__(256) anchor_pick_kernel(AnchorArgs a) {
+constexpr int kPickThreads = 512;
+
+__global__ void __launch_bounds__(kPickThreads) anchor_pick_kernel(AnchorArgs a) {
+  constexpr int kHB = 8;                       // heads whose scores are loaded together
+  constexpr int kNW = kPickThreads / kWave;
   __shared__ float Mh[64], Lh[64];
-  __shared__ float bv[4];
-  __shared__ int bi[4];
+  __shared__ float bv[kNW];
+  __shared__ int bi[kNW];
   const int b = blockIdx.x, tid = threadIdx.x;
   const SeqDesc s = a.seqs[b];
   const int acc = a.accept_len[b];
@@ -115,10 +119,10 @@ __global__ void __launch_bounds__(256) anchor_pick_kernel(AnchorArgs a) {
     }
     return;
   }
-  const int T = s.T, nch = (T + kAnchorChunk - 1) / kAnchorChunk;
+  const int T = s.T, H = a.H, nch = (T + kAnchorChunk - 1) / kAnchorChunk;
   // each head's softmax normaliser from its chunks, in chunk order
-  for (int h = tid; h < a.H; h += blockDim.x) {
-    const float2* st = a.stats + ((size_t)b * a.H + h) * a.nchunks;
+  for (int h = tid; h < H; h += kPickThreads) {
+    const float2* st = a.stats + ((size_t)b * H + h) * a.nchunks;
     float M = -INFINITY;
     for (int c = 0; c < nch; ++c) M = fmaxf(M, st[c].x);
     float L = 0.f;
@@ -127,18 +131,37 @@ __global__ void __launch_bounds__(256) anchor_pick_kernel(AnchorArgs a) {
     Lh[h] = L;
   }
   __syncthreads();
-  // head-averaged weight per frame; this thread's best (frames rise, so '>' keeps the
-  // lowest index among equal values)
-  const float* sc = a.score + (size_t)b * a.H * a.max_frames;
+  // head-averaged weight per frame (heads summed in order), two frames per pass and
+  // eight heads' scores per round of loads; this thread's best (its frames rise, so
+  // '>' keeps the lowest index among equal values)
+  const float* sc = a.score + (size_t)b * H * a.max_frames;
   float best = -1.f;
   int best_t = 0x7fffffff;
-  for (int t = tid; t < T; t += blockDim.x) {
-    float w = 0.f;
-    for (int h = 0; h < a.H; ++h) w += expf(sc[(size_t)h * a.max_frames + t] - Mh[h]) / Lh[h];
-    w = w / (float)a.H;
-    if (w > best) {
-      best = w;
-      best_t = t;
+  for (int t0 = tid; t0 < T; t0 += 2 * kPickThreads) {
+    float w[2] = {0.f, 0.f};
+    for (int hb = 0; hb < H; hb += kHB) {
+      float v[2][kHB];
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int e = 0; e < kHB; ++e) {
+          const int h = min(hb + e, H - 1), t = min(t0 + f * kPickThreads, T - 1);
+          v[f][e] = sc[(size_t)h * a.max_frames + t];
+        }
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int e = 0; e < kHB; ++e)
+          if (hb + e < H) w[f] += expf(v[f][e] - Mh[hb + e]) / Lh[hb + e];
+    }
+#pragma unroll
+    for (int f = 0; f < 2; ++f) {
+      const int t = t0 + f * kPickThreads;
+      const float wt = w[f] / (float)H;
+      if (t < T && wt > best) {
+        best = wt;
+        best_t = t;
+      }
     }
   }
   // block argmax: larger value, then lower frame
@@ -158,7 +181,7 @@ __global__ void __launch_bounds__(256) anchor_pick_kernel(AnchorArgs a) {
   if (tid == 0) {
     float v = bv[0];
     int t = bi[0];
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < kNW; ++w)
       if ((bv[w] > v) | ((bv[w] == v) & (bi[w] < t))) {
         v = bv[w];
         t = bi[w];
@@ -180,7 +203,7 @@ size_t anchor_scratch_floats(int B, int H, int max_frames) {
 template <class S>
 void launch_anchor(const AnchorArgs& a, int B, hipStream_t st) {
   hipLaunchKernelGGL(anchor_scores_kernel<S>, dim3(a.H, B, a.nchunks), dim3(256), 0, st, a);
-  hipLaunchKernelGGL(anchor_pick_kernel, dim3(B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(anchor_pick_kernel, dim3(B), dim3(kPickThreads), 0, st, a);
 }
 template void launch_anchor<F32>(const AnchorArgs&, int, hipStream_t);
 template void launch_anchor<BF16>(const AnchorArgs&, int, hipStream_t);
