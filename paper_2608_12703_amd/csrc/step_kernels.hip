@@ -151,6 +151,42 @@ __device__ __forceinline__ float row_block_sum(float v, float* red) {
   return t;
 }
 
+// split_sum4 with the first eight planes as straight-line loads (planes past nsplit
+// are clamped reads that add -0, which leaves every value, signed zeros included,
+// unchanged): no loop, so loads issued before it stay in flight across it.  Further
+// planes, if any, in a loop.
+__device__ __forceinline__ float4 split_sum4_flat(const float* P, size_t plane, size_t e, int nsplit) {
+  float4 p[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) p[u] = *(const float4*)(P + (size_t)min(u, nsplit - 1) * plane + e);
+  float4 acc = p[0];
+#pragma unroll
+  for (int u = 1; u < 8; ++u) {
+    const bool in = u < nsplit;
+    acc.x += in ? p[u].x : -0.f;
+    acc.y += in ? p[u].y : -0.f;
+    acc.z += in ? p[u].z : -0.f;
+    acc.w += in ? p[u].w : -0.f;
+  }
+  for (int t = 8; t < nsplit; ++t) {
+    const float4 w = *(const float4*)(P + (size_t)t * plane + e);
+    acc.x += w.x; acc.y += w.y; acc.z += w.z; acc.w += w.w;
+  }
+  return acc;
+}
+
+// The same for a `red` array that no other reduction of the kernel uses (no barrier
+// needed before writing it).
+__device__ __forceinline__ float row_block_sum_once(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
 __device__ __forceinline__ float4 ld_bf16x4(const uint16_t* p, int j) {
   const uint2 u = *(const uint2*)(p + j);
   return float4{bf16_to_f32(u.x & 0xffff), bf16_to_f32(u.x >> 16), bf16_to_f32(u.y & 0xffff),
@@ -179,24 +215,28 @@ __global__ void __launch_bounds__(1024) reduce_res_ln_kernel(int M, int d, int n
                                                              float* x, const uint16_t* g,
                                                              const uint16_t* b, uint16_t* frag,
                                                              int RT, float* out) {
-  __shared__ float red[16];
+  __shared__ float red_mean[16], red_var[16];
   const int m = blockIdx.x, j = threadIdx.x * 4;
   const bool on = j < d;
-  const size_t e = (size_t)m * d + (on ? j : 0);
+  const int jc = on ? j : 0;
+  const size_t e = (size_t)m * d + jc;
+  // every load of the row up front (one round trip): partials, bias, residual, and the
+  // LayerNorm gain and shift
+  const float4 bb = ld_bf16x4(bias, jc);
+  const float4 x0 = *(const float4*)(x + e);
+  const float4 gv = ld_bf16x4(g, jc), bv = ld_bf16x4(b, jc);
+  const float4 v = split_sum4_flat(P, (size_t)M * d, e, nsplit);
   float4 xv{0.f, 0.f, 0.f, 0.f};
   if (on) {
-    const float4 v = split_sum4(P, (size_t)M * d, e, nsplit);
-    const float4 bv = ld_bf16x4(bias, j);
-    xv = *(const float4*)(x + e);
-    xv.x += v.x + bv.x; xv.y += v.y + bv.y; xv.z += v.z + bv.z; xv.w += v.w + bv.w;
+    xv = x0;
+    xv.x += v.x + bb.x; xv.y += v.y + bb.y; xv.z += v.z + bb.z; xv.w += v.w + bb.w;
     *(float4*)(x + e) = xv;
   }
-  const float mean = row_block_sum(on ? (xv.x + xv.y) + (xv.z + xv.w) : 0.f, red) / (float)d;
+  const float mean = row_block_sum_once(on ? (xv.x + xv.y) + (xv.z + xv.w) : 0.f, red_mean) / (float)d;
   const float4 c{xv.x - mean, xv.y - mean, xv.z - mean, xv.w - mean};
-  const float var = row_block_sum(on ? (c.x * c.x + c.y * c.y) + (c.z * c.z + c.w * c.w) : 0.f, red);
+  const float var = row_block_sum_once(on ? (c.x * c.x + c.y * c.y) + (c.z * c.z + c.w * c.w) : 0.f, red_var);
   const float rstd = 1.0f / sqrtf(var / (float)d + 1e-5f);
   if (on) {
-    const float4 gv = ld_bf16x4(g, j), bv = ld_bf16x4(b, j);
     const float4 y{c.x * rstd * gv.x + bv.x, c.y * rstd * gv.y + bv.y, c.z * rstd * gv.z + bv.z,
                    c.w * rstd * gv.w + bv.w};
     afrag_store4(frag, RT, m, j, y);
