@@ -3,10 +3,14 @@
 // C[m][n] = sum_k X[m][k] W[n][k] with W bf16 [N][K] and X float32 activations stored as
 // a hi/lo bf16 pair in A-fragment order.  A workgroup owns 128 output columns and up to
 // RTC 16-row tiles; its eight waves (two per SIMD, so one wave's LDS reads overlap the
-// other's matrix instructions) each own a quarter of the rows and half of the columns.  Operands move in 32-wide K steps through LDS rings filled by direct
-// global->LDS loads: activations (L2-resident) two steps ahead, weights (streamed from
-// HBM) five steps ahead.  The waits are explicit; the loop is unrolled over the ring
-// stages so every buffer is a distinct LDS object.  Small-N products split K over several
+// other's matrix instructions) each own a quarter of the rows and half of the columns.
+// Weights (streamed from HBM) move in 32-wide K steps through an LDS ring filled by
+// direct global->LDS loads five steps ahead.  Activations (L2-resident) go straight into
+// a register ring five steps ahead for tiles of up to 8 row tiles (the A-fragment order
+// is the matrix instruction's lane order, so each is one coalesced 16-byte load per
+// lane; keeping them out of LDS removes a third of the step's LDS traffic), and through
+// a three-stage LDS ring for 16 row tiles.  The waits are explicit; the loop is unrolled
+// over the ring stages so every buffer is a distinct object.  Small-N products split K over several
 // workgroups and the last one to finish a tile sums the partial tiles in split order.
 // The split count depends on the weight shape only, so a row's result never depends
 // on how many other rows share the launch.
@@ -103,6 +107,31 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][4], const uint4* 
   }
 }
 
+// The activation operand of one K step for the RW row tiles of one wave, in registers.
+template <int RW>
+struct AFrag {
+  uint4 h[RW], l[RW];
+};
+
+// One 32-wide K step with the activations from registers.
+template <int RTC>
+__device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RTC / 4][4], const AFrag<RTC / 4>& a,
+                                             const uint4* wbuf, int ch, int lane) {
+  constexpr int RW = RTC / 4;
+  bf16x8 b[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) b[ct] = as_bf16x8(wbuf[(ch * 4 + ct) * 64 + lane]);
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    const bf16x8 ah = as_bf16x8(a.h[r]), al = as_bf16x8(a.l[r]);
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
+      acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
+    }
+  }
+}
+
 template <int EPI, int RTC, bool PACKED>
 __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   constexpr int RW = RTC / 4;            // row tiles per wave
@@ -155,7 +184,60 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     }
   };
   int kb = kb0;
-  {
+  if constexpr (RTC <= 8) {
+    // Activations straight into registers (the A-fragment layout is the matrix
+    // instruction's lane order, so each is one coalesced 16-byte load per lane), five
+    // steps ahead like the weights: only the weights pass through LDS, which halves the
+    // LDS traffic of a step.  Step j requests A(j+5) then W(j+5); at the end of step j
+    // the loads issued after W(j+1) are four (A, W) pairs, so the barrier's wait also
+    // completes A(j+1) and the compiler needs no wait of its own for the registers.
+    constexpr int kA = 2 * RW;                       // activation loads per step
+    constexpr int kWait = 4 * (kA + 1);
+    const uint4* abase = (const uint4*)g.A + ((size_t)rt0 + rg * RW) * 128 + lane;
+    auto la = [&](AFrag<RW>& f, int k) {
+      const uint4* src = abase + (size_t)min(k, kl) * g.RT * 128;
+#pragma unroll
+      for (int r = 0; r < RW; ++r) {
+        f.h[r] = src[(r * 2 + 0) * 64];
+        f.l[r] = src[(r * 2 + 1) * 64];
+      }
+    };
+    AFrag<RW> a0, a1, a2, a3, a4, a5;
+    la(a0, kb0);
+    iw(sw0, kb0);
+    la(a1, kb0 + 1);
+    iw(sw1, kb0 + 1);
+    la(a2, kb0 + 2);
+    iw(sw2, kb0 + 2);
+    la(a3, kb0 + 3);
+    iw(sw3, kb0 + 3);
+    la(a4, kb0 + 4);
+    iw(sw4, kb0 + 4);
+    BARRIER_VMCNT(kWait);
+#define GEMM_STEP(CA, CW, NXA, NXW)                 \
+  {                                                 \
+    la(NXA, kb + 5);                                \
+    iw(NXW, kb + 5);                                \
+    mma_step_reg<RTC>(acc, CA, CW, ch, lane);       \
+    BARRIER_VMCNT(kWait);                           \
+    ++kb;                                           \
+  }
+    for (int it = 0; it < nk / 6; ++it) {
+      GEMM_STEP(a0, sw0, a5, sw5)
+      GEMM_STEP(a1, sw1, a0, sw0)
+      GEMM_STEP(a2, sw2, a1, sw1)
+      GEMM_STEP(a3, sw3, a2, sw2)
+      GEMM_STEP(a4, sw4, a3, sw3)
+      GEMM_STEP(a5, sw5, a4, sw4)
+    }
+    const int rem = nk % 6;
+    if (rem >= 1) GEMM_STEP(a0, sw0, a5, sw5)
+    if (rem >= 2) GEMM_STEP(a1, sw1, a0, sw0)
+    if (rem >= 3) GEMM_STEP(a2, sw2, a1, sw1)
+    if (rem >= 4) GEMM_STEP(a3, sw3, a2, sw2)
+    if (rem >= 5) GEMM_STEP(a4, sw4, a3, sw3)
+#undef GEMM_STEP
+  } else {
     // Step j requests activations j + 2 and weights j + 5, in that order; the prologue
     // plays virtual steps -5 .. -1 so the outstanding-load count is the same everywhere:
     // at the end of step j the loads issued after A(j+1) are W(j+4), A(j+2), W(j+5).
