@@ -147,17 +147,26 @@ class BlockOut:
     hidden: np.ndarray      # [r, d] final-LN output
     new_kv: list            # per layer (K, V) of the block rows, [r, H, 64], stored
     xattn: np.ndarray | None = None   # [r, H, T] cross-attention weights at the probed layer
+    taps: np.ndarray | None = None    # [n_taps, r, d] residual stream after the tapped layers
 
 
-def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None = None) -> BlockOut:
+def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None = None,
+                  in_rows=None, cross_window=None, taps=None) -> BlockOut:
     """One causal decoder pass over ``tokens`` placed at positions n..n+r-1.  With
-    ``probe_layer`` set, also returns that layer's cross-attention weights."""
+    ``probe_layer`` set, also returns that layer's cross-attention weights.
+
+    in_rows [r, d]: replaces the token embedding of the rows (the position embedding is
+    still added).  cross_window (lo, hi): the rows attend to frames lo..hi-1 only.
+    taps: list of layer indices; the residual stream after each is returned in
+    ``BlockOut.taps`` [len(taps), r, d]."""
     tokens = np.asarray(tokens, dtype=np.int64)
     r, n, d, H = len(tokens), state.n, model.d, model.H
     if n + r > MAX_POS:
         raise ValueError("block runs past the last decoder position")
     pos = n + np.arange(r)
-    x = model.w("tok_emb")[tokens] + model.w("pos_emb")[pos]
+    emb = model.w("tok_emb")[tokens] if in_rows is None else np.asarray(in_rows, np.float64)
+    x = emb + model.w("pos_emb")[pos]
+    tapped = {}
     new_kv = []
     xattn = None
     for layer in range(model.L):
@@ -174,6 +183,8 @@ def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None
         h = layer_norm(x, model.lw(layer, "ln2_g"), model.lw(layer, "ln2_b"))
         q = (h @ model.lw(layer, "w_xq").T + model.lw(layer, "b_xq")).reshape(r, H, HEAD)
         Kx, Vx = state.cross[layer]
+        if cross_window is not None:
+            Kx, Vx = Kx[cross_window[0]: cross_window[1]], Vx[cross_window[0]: cross_window[1]]
         a = attention(q, Kx, Vx, visible=np.full(r, Kx.shape[0])).reshape(r, d)
         if layer == probe_layer:
             xattn = attention_probs(q, Kx, visible=np.full(r, Kx.shape[0]))
@@ -183,9 +194,11 @@ def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None
         u = gelu(h @ model.lw(layer, "w_1").T + model.lw(layer, "b_1"))
         x = x + u @ model.lw(layer, "w_2").T + model.lw(layer, "b_2")
         new_kv.append((k, v))
+        tapped[layer] = x.copy()
     hidden = layer_norm(x, model.w("lnf_g"), model.w("lnf_b"))
     logits = hidden @ model.w("tok_emb").T
-    return BlockOut(logits, hidden, new_kv, xattn)
+    tap_out = None if taps is None else np.stack([tapped[t] for t in taps])
+    return BlockOut(logits, hidden, new_kv, xattn, tap_out)
 
 
 # ---------------------------------------------------------------------- verify / AR

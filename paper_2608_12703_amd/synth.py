@@ -34,7 +34,7 @@ import numpy as np
 from .configs import Config, HEAD_DIM, MAX_POS, SOT_TOKEN
 
 # stream ids (fixed order; never renumber)
-S_WEIGHTS, S_ENCODER, S_KVLEN, S_PREFIX, S_GEO, S_FILL, S_ANCHOR, S_HEADS, S_SHAPE = range(9)
+S_WEIGHTS, S_ENCODER, S_KVLEN, S_PREFIX, S_GEO, S_FILL, S_ANCHOR, S_HEADS, S_SHAPE, S_DRAFT = range(10)
 
 
 def _rng(seed: int, stream: int, index: int) -> np.random.Generator:
@@ -109,6 +109,45 @@ def make_draft_heads(cfg: Config, seed: int | None = None) -> np.ndarray:
         out[i] = _rng(seed, S_HEADS, i).standard_normal((cfg.vocab, cfg.d_model),
                                                          dtype=np.float32) * np.float32(0.02)
     return _store(out, cfg.dtype)
+
+
+def draft_config(cfg: Config) -> Config:
+    """The audio-conditioned draft block of a target: one decoder layer of the target's
+    width and heads with a feed-forward width of twice the model width (the paper's
+    drafts use 1024/2048 and 2048/4096)."""
+    return cfg.with_(name=cfg.name + "_draft", n_layers=1, d_ffn=2 * cfg.d_model)
+
+
+DRAFT_EXTRA = ("w_fuse", "b_fuse", "w_in", "b_in")
+
+
+def draft_param_specs(cfg: Config):
+    """(name, shape) of the draft's own parameters: the block (layer 0) and its final
+    LayerNorm in the C-ABI order of a one-layer model (the token and position tables are
+    the target's), then the input projections: w_fuse [d, 4d] maps four target
+    representations to one feature, w_in [d, 2d] maps (feature, token embedding) to the
+    block's input."""
+    dc, d = draft_config(cfg), cfg.d_model
+    specs = [(n, sh) for n, sh in param_specs(dc) if n not in ("tok_emb", "pos_emb")]
+    return specs + [("w_fuse", (d, 4 * d)), ("b_fuse", (d,)), ("w_in", (d, 2 * d)), ("b_in", (d,))]
+
+
+def make_draft_params(cfg: Config, seed: int | None = None) -> dict:
+    """Random-init draft parameters (N(0, 0.02); LayerNorm gains 1 + N(0, 0.02))."""
+    seed = cfg.seed if seed is None else seed
+    out = {}
+    for i, (name, shape) in enumerate(draft_param_specs(cfg)):
+        g = _rng(seed, S_DRAFT, i)
+        x = g.standard_normal(shape, dtype=np.float32) * np.float32(0.02)
+        if name.split(".")[-1].endswith("_g"):
+            x += np.float32(1.0)
+        d = cfg.d_model
+        if name.split(".")[-1] == "b_qkv":
+            x[d: 2 * d] = 0.0                # keys carry no bias, as in the target
+        if name.split(".")[-1] == "b_xkv":
+            x[:d] = 0.0
+        out[name] = _store(x, cfg.dtype)
+    return out
 
 
 # --------------------------------------------------------------------- per-sequence data
