@@ -185,6 +185,18 @@ typedef struct {
   int32_t anchor_layer;
   int32_t* out_anchor;        /* device [B] out                                      */
   float* out_anchor_peak;     /* device [B] out (optional)                           */
+  /* Running the audio-conditioned draft block (see ad_draft_input), all optional:
+   * in_rows replaces every row's token embedding (the position embedding of the row's
+   * position is still added; tokens are still validated and scanned); cross_window[b] =
+   * {lo, hi} restricts sequence b's cross-attention to frames lo .. hi - 1 (0 <= lo < hi
+   * <= T_b, else AD_ERR_FRAMES; the anchor readout always covers every frame); out_taps
+   * receives, for each tap_layers[i] >= 0, the residual stream after that layer at every
+   * row (the four target representations the draft reads are these three and
+   * out_hidden).                                                                     */
+  const float* in_rows;       /* device [rows][d_model] (optional)                   */
+  const int32_t* cross_window; /* device [B][2] (optional)                           */
+  int32_t tap_layers[3];      /* layer indices, -1 for none                          */
+  float* out_taps;            /* device [3][rows][d_model] out (optional)            */
 } ad_step;
 
 /* Bytes of workspace a step with up to max_rows rows, max_batch sequences and draft
@@ -215,6 +227,37 @@ ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_c
  * Errors: AD_EINVAL, AD_ERANGE, AD_ENOSPACE, AD_EHIP (see conventions above).
  */
 ad_status ad_verify_step(const ad_model* model, const ad_step* step, void* stream);
+
+/*
+ * Input rows of the audio-conditioned draft block (paper, section 3 "Models and
+ * Protocol": the draft follows EAGLE-3 and adds cross-attention to the audio encoder;
+ * appendix "Draft architecture": four frozen target representations combined with the
+ * current token embedding, then one causal block).  For every sequence b
+ *   out[b] = W_in [f_b ; E_tok[t_b]] + b_in                         (float32 [B][d])
+ * where f_b = W_fuse [taps_0 ; taps_1 ; taps_2 ; hidden] + b_fuse at sequence b's last
+ * verified row of a target step when `taps` is given (a round's first draft step; the
+ * row is row accept_len[b] of the step's layout, described by layout / k_max / cu_rows /
+ * rows; taps is the step's out_taps [3][rows][d] and hidden its out_hidden), else
+ * f_b = feature[b] (later steps: the draft block's previous out_hidden row, [B][d]).
+ * t_b = tokens[b * token_stride + (token_index ? token_index[b] : 0)]; a round's first
+ * token is the target step's out_tokens[b][a_b] (tokens = out_tokens, token_stride =
+ * k_max + 1, token_index = accept_len).  With `anchor` given, window[b] receives
+ * {max(0, c - half_window), min(T_b, c + half_window + 1)} around c = anchor[b] (the
+ * verification-attention anchor; T_b from enc_len), the draft block's cross_window.
+ * W_fuse [d][4d], W_in [d][2d], b_fuse, b_in: device arrays of the target's dtype; the
+ * token table is the target's.  Skipped sequences (accept_len < 0) get zero features.
+ * Errors: AD_EINVAL (NULL argument, bad layout), AD_ERANGE (batch < 1, rows < batch,
+ * token_stride < 1, half_window < 0), AD_ENOSPACE (workspace too small).
+ */
+ad_status ad_draft_input_workspace_size(const ad_model* target, int32_t batch, size_t* bytes);
+ad_status ad_draft_input(const ad_model* target, const void* w_fuse, const void* b_fuse,
+                         const void* w_in, const void* b_in, int32_t batch, const float* taps,
+                         const float* hidden, int32_t layout, int32_t k_max,
+                         const int32_t* cu_rows, const int32_t* accept_len, int32_t rows,
+                         const float* feature, const int32_t* tokens, int32_t token_stride,
+                         const int32_t* token_index, const int32_t* anchor,
+                         const int32_t* enc_len, int32_t half_window, int32_t* window,
+                         float* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Commit / roll back (appendix "Real cached loop"): kv_len[b] += accept_len[b] + 1 for

@@ -45,7 +45,9 @@ class Step(ctypes.Structure):
                 ("accept_len", _ptr), ("out_tokens", _ptr), ("out_greedy", _ptr),
                 ("out_logits", _ptr), ("out_hidden", _ptr), ("out_margin", _ptr),
                 ("err_flag", _ptr), ("workspace", _ptr), ("workspace_bytes", _size),
-                ("anchor_layer", _i32), ("out_anchor", _ptr), ("out_anchor_peak", _ptr)]
+                ("anchor_layer", _i32), ("out_anchor", _ptr), ("out_anchor_peak", _ptr),
+                ("in_rows", _ptr), ("cross_window", _ptr), ("tap_layers", _i32 * 3),
+                ("out_taps", _ptr)]
 
 
 def _load():
@@ -68,6 +70,10 @@ def _load():
         "ad_draft_heads": (_i32, [_ptr, _ptr, _i32, _ptr, _i32, _i32, _ptr, _ptr, _ptr, _i32,
                                   _ptr, _ptr, _size, _ptr]),
         "ad_kv_import": (_i32, [_ptr, ctypes.POINTER(KV), _i32, _ptr, _i32, _ptr, _ptr]),
+        "ad_draft_input_workspace_size": (_i32, [_ptr, _i32, ctypes.POINTER(_size)]),
+        "ad_draft_input": (_i32, [_ptr, _ptr, _ptr, _ptr, _ptr, _i32, _ptr, _ptr, _i32, _i32, _ptr,
+                                  _ptr, _i32, _ptr, _ptr, _i32, _ptr, _ptr, _ptr, _i32, _ptr, _ptr,
+                                  _ptr, _size, _ptr]),
         "ad_kv_export": (_i32, [_ptr, ctypes.POINTER(KV), _i32, _ptr, _i32, _ptr, _ptr]),
         "ad_profile_enable": (_i32, [_ptr, _i32, _i32]),
         "ad_profile_read": (_i32, [_ptr, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i32)]),
@@ -83,6 +89,7 @@ EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model
            "ad_model_pack_size", "ad_model_pack",
            "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
+           "ad_draft_input_workspace_size", "ad_draft_input",
            "ad_profile_enable", "ad_profile_read")
 PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD, PROF_XQ_CROSS, PROF_XQ, PROF_ANCHOR = 1, 2, 3, 4, 5, 6, 7
 
@@ -189,6 +196,24 @@ def draft_heads(model: Model, heads_w, n_heads: int, hidden, layout: int, k_max:
                              ptr(cu_rows), ptr(accept_len), ptr(out_tokens), batch,
                              ptr(next_tokens), ptr(workspace), workspace.numel(),
                              stream_handle(stream)), "ad_draft_heads")
+
+
+def draft_input_workspace_size(model: Model, batch: int) -> int:
+    n = _size()
+    check(LIB.ad_draft_input_workspace_size(model.handle, batch, ctypes.byref(n)),
+          "ad_draft_input_workspace_size")
+    return n.value
+
+
+def draft_input(model: Model, w_fuse, b_fuse, w_in, b_in, batch: int, taps, hidden, layout: int,
+                k_max: int, cu_rows, accept_len, rows: int, feature, tokens, token_stride: int,
+                token_index, anchor, enc_len, half_window: int, window, out, workspace, stream=None):
+    check(LIB.ad_draft_input(model.handle, ptr(w_fuse), ptr(b_fuse), ptr(w_in), ptr(b_in), batch,
+                             ptr(taps), ptr(hidden), layout, k_max, ptr(cu_rows), ptr(accept_len),
+                             rows, ptr(feature), ptr(tokens), token_stride, ptr(token_index),
+                             ptr(anchor), ptr(enc_len), half_window, ptr(window), ptr(out),
+                             ptr(workspace), workspace.numel(), stream_handle(stream)),
+          "ad_draft_input")
 
 
 def kv_import(model: Model, kv: KV, b: int, src, n: int, err_flag, stream=None):

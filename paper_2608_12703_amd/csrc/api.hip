@@ -160,6 +160,15 @@ struct ProfScope {
   ~ProfScope() { stop(); }
 };
 
+// The residual stream after layer l into the step's tap slots that name it.
+void copy_taps(const ad_step* s, int l, const float* x, int M, int d, hipStream_t st) {
+  if (!s->out_taps) return;
+  for (int i = 0; i < 3; ++i)
+    if (s->tap_layers[i] == l)
+      (void)hipMemcpyAsync(s->out_taps + (size_t)i * M * d, x, sizeof(float) * M * d,
+                           hipMemcpyDeviceToDevice, st);
+}
+
 ad::AnchorArgs anchor_args(const ad_model* m, const ad_step* s, const Workspace& w) {
   const ad_model_desc& D = m->desc;
   ad::AnchorArgs a{};
@@ -187,9 +196,9 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
                  s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
                  s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
-                 s->cross.frames_cap};
+                 s->cross.frames_cap, s->cross_window};
   ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
-  ad::launch_embed<S>(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, st);
+  ad::launch_embed<S>(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, s->in_rows, st);
 
   ad::EpiArgs e{};
   e.rows = w.rows;
@@ -231,6 +240,7 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     ad::launch_gemm_valu<S>(ad::EPI_GELU, M, F, d, w.ln, lp(m, l, W_1), lp(m, l, B_1), e, st);
     e.out = w.x; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, F, w.hid, lp(m, l, W_2), lp(m, l, B_2), e, st);
+    copy_taps(s, l, w.x, M, d, st);
   }
   float* hidden = s->out_hidden ? s->out_hidden : w.hidden;
   ad::launch_layernorm<S>(M, d, w.x, m->p[P_LNF_G], m->p[P_LNF_B], hidden, st);
@@ -256,10 +266,10 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
                  s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
                  s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
-                 s->cross.frames_cap};
+                 s->cross.frames_cap, s->cross_window};
   ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
-  ad::launch_embed_ln(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, lp(m, 0, LN1_G), lp(m, 0, LN1_B),
-                      w.afrag, RT, st);
+  ad::launch_embed_ln(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, s->in_rows, lp(m, 0, LN1_G),
+                      lp(m, 0, LN1_B), w.afrag, RT, st);
 
   const std::vector<size_t>& poff = m->pack_off;
   // weight `which` of layer l (layer -1: the LM head), tiled when the model is packed
@@ -336,6 +346,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
                              last ? m->p[P_LNF_G] : lp(m, l + 1, LN1_G),
                              last ? m->p[P_LNF_B] : lp(m, l + 1, LN1_B), w.afrag, RT,
                              last ? hidden : nullptr, st);
+    copy_taps(s, l, w.x, M, d, st);
   }
   ad::EpiArgs e{};
   e.out = s->out_logits; e.ldo = V; e.am_part = w.ampart;
@@ -525,6 +536,11 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
     return fail(AD_ERANGE, "anchor_layer must be -1 or a layer index");
   if (s->anchor_layer >= 0 && !s->out_anchor)
     return fail(AD_EINVAL, "the anchor readout needs out_anchor");
+  for (int i = 0; i < 3; ++i) {
+    if (s->tap_layers[i] < -1 || s->tap_layers[i] >= D.n_layers)
+      return fail(AD_ERANGE, "tap_layers must be -1 or layer indices");
+    if (s->tap_layers[i] >= 0 && !s->out_taps) return fail(AD_EINVAL, "tap_layers need out_taps");
+  }
   const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");
@@ -534,6 +550,64 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (D.dtype == AD_BF16) run_step_mfma(model, s, w, st);
   else run_step_valu<ad::F32>(model, s, w, st);
   return check_hip("ad_verify_step");
+}
+
+ad_status ad_draft_input_workspace_size(const ad_model* model, int32_t batch, size_t* bytes) {
+  if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
+  if (batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
+  *bytes = sizeof(float) * 7 * (size_t)model->desc.d_model * batch;
+  return AD_OK;
+}
+
+ad_status ad_draft_input(const ad_model* model, const void* w_fuse, const void* b_fuse,
+                         const void* w_in, const void* b_in, int32_t batch, const float* taps,
+                         const float* hidden, int32_t layout, int32_t k_max,
+                         const int32_t* cu_rows, const int32_t* accept_len, int32_t rows,
+                         const float* feature, const int32_t* tokens, int32_t token_stride,
+                         const int32_t* token_index, const int32_t* anchor,
+                         const int32_t* enc_len, int32_t half_window, int32_t* window,
+                         float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!model || !w_fuse || !b_fuse || !w_in || !b_in || !tokens || !out || !workspace)
+    return fail(AD_EINVAL, "NULL argument");
+  if (batch < 1 || token_stride < 1) return fail(AD_ERANGE, "batch and token_stride must be >= 1");
+  if (taps) {
+    if (!hidden || !accept_len) return fail(AD_EINVAL, "taps need hidden and accept_len");
+    if (layout != AD_PADDED && layout != AD_PACKED) return fail(AD_EINVAL, "unknown layout");
+    if (layout == AD_PACKED && !cu_rows) return fail(AD_EINVAL, "packed layout needs cu_rows");
+    if (rows < batch || k_max < 0) return fail(AD_ERANGE, "rows must be >= batch, k_max >= 0");
+  } else if (!feature) {
+    return fail(AD_EINVAL, "either taps or feature is needed");
+  }
+  if (anchor && (!enc_len || !window)) return fail(AD_EINVAL, "anchor needs enc_len and window");
+  if (anchor && half_window < 0) return fail(AD_ERANGE, "half_window must be >= 0");
+  const ad_model_desc& D = model->desc;
+  const int d = D.d_model;
+  size_t need = 0;
+  ad_draft_input_workspace_size(model, batch, &need);
+  if (workspace_bytes < need) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need) + " bytes");
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  float* taps4 = (float*)workspace;
+  float* feat = taps4 + (size_t)4 * d * batch;
+  float* z = feat + (size_t)d * batch;
+  const float* f = feature;
+  ad::EpiArgs e{};
+  e.ldo = d;
+  const bool bf16 = D.dtype == AD_BF16;
+  if (taps) {
+    ad::launch_draft_gather_taps(batch, d, layout, k_max, cu_rows, accept_len, rows, taps, hidden,
+                                 taps4, st);
+    e.out = feat;
+    if (bf16) ad::launch_gemm_valu<ad::BF16>(ad::EPI_STORE, batch, d, 4 * d, taps4, w_fuse, b_fuse, e, st);
+    else ad::launch_gemm_valu<ad::F32>(ad::EPI_STORE, batch, d, 4 * d, taps4, w_fuse, b_fuse, e, st);
+    f = feat;
+  }
+  ad::launch_draft_concat(batch, d, f, model->p[P_TOK], bf16, tokens, token_stride, token_index, z, st);
+  e.out = out;
+  if (bf16) ad::launch_gemm_valu<ad::BF16>(ad::EPI_STORE, batch, d, 2 * d, z, w_in, b_in, e, st);
+  else ad::launch_gemm_valu<ad::F32>(ad::EPI_STORE, batch, d, 2 * d, z, w_in, b_in, e, st);
+  if (anchor) ad::launch_draft_window(batch, anchor, enc_len, half_window, window, st);
+  return check_hip("ad_draft_input");
 }
 
 ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch, void* stream) {

@@ -194,7 +194,7 @@ struct SeqDesc {
   int T;        // encoder frames
   int enc_off;  // first cross-KV slot
   int valid;    // 0 -> skipped (error bits were raised)
-  int pad0, pad1;
+  int wlo, whi; // cross-attention frames [wlo, whi) (0, T unless a window is given)
 };
 
 struct RowDesc {

@@ -22,6 +22,7 @@ struct StepArgs {
   const int* enc_len;
   const int* enc_off;
   int frames_cap;
+  const int* cross_window;   // [B][2] frames [lo, hi), or NULL: all frames
 };
 
 // Where a GEMM's epilogue sends its output.
@@ -49,9 +50,10 @@ struct EpiArgs {
 };
 
 void launch_prep(const StepArgs& a, SeqDesc* seqs, RowDesc* rows, int* err, hipStream_t st);
+// x = E_tok[token] + E_pos[pos] per row, or in_rows[row] + E_pos[pos] when in_rows is set.
 template <class S>
 void launch_embed(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
-                  hipStream_t st);
+                  const float* in_rows, hipStream_t st);
 template <class S>
 void launch_layernorm(int M, int d, const float* x, const void* g, const void* b, float* out,
                       hipStream_t st);
@@ -160,9 +162,22 @@ void launch_zero_i32(int* p, int n, hipStream_t st);
 void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* bias, float* x,
                           const void* g, const void* b, uint16_t* frag, int RT, float* out,
                           hipStream_t st);
-// bf16 model: embedding fused with the first LayerNorm.
+// bf16 model: embedding (or in_rows, as in launch_embed) fused with the first LayerNorm.
 void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
-                     const void* g, const void* b, uint16_t* frag, int RT, hipStream_t st);
+                     const float* in_rows, const void* g, const void* b, uint16_t* frag, int RT,
+                     hipStream_t st);
+// Draft-block input rows: Z[b] = [f_b ; E_tok[token_b]] with f_b either the fused target
+// features (computed by the caller into feat) or the previous step's output; and the
+// four target representations of sequence b's last verified row gathered into
+// taps4[b] = [taps_0 ; taps_1 ; taps_2 ; hidden] (see ad_draft_input).
+void launch_draft_gather_taps(int B, int d, int layout, int k_max, const int* cu_rows,
+                              const int* accept_len, int rows, const float* taps,
+                              const float* hidden, float* taps4, hipStream_t st);
+void launch_draft_concat(int B, int d, const float* feat, const void* tok_emb, int bf16,
+                         const int* tokens, int token_stride, const int* token_index, float* z,
+                         hipStream_t st);
+void launch_draft_window(int B, const int* anchor, const int* enc_len, int half, int* window,
+                         hipStream_t st);
 
 // Attention of every block row over the paged self cache (causal inside the block) or
 // over the sequence's encoder frames.  q and out are float32 [rows][d].

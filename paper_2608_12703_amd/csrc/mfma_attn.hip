@@ -68,7 +68,10 @@ __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, 
                                            KVTiles& t) {
   if (CROSS) {
     // one 32-frame block: keys and values already in operand order, 1 KB per load
-    const int b0 = blk < k_end ? blk : k_beg + (k_end - 1 - k_beg) / kCrossBlock * kCrossBlock;
+    // (a chunk wholly before a cross-attention window has k_end <= k_beg: it reloads its
+    // first block, which lies inside the sequence's slots)
+    const int b0 = blk < k_end ? blk
+                               : (k_end > k_beg ? k_beg + (k_end - 1 - k_beg) / kCrossBlock * kCrossBlock : k_beg);
     const size_t bo = (size_t)((s.enc_off + b0) / kCrossBlock) * 2 * kCrossBlockElems + (grp * 16 + c16) * 8;
     const uint16_t* kp = a.kv + cross_base(a.layer, h, a.H, a.frames_cap) + bo;
     const uint16_t* vp = kp + kCrossBlockElems;
@@ -115,7 +118,7 @@ __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, 
 // never reach the output).  Unmasked blocks skip all of that.  Queries past the group
 // (zero rows) are computed but never stored.
 template <bool MASKED>
-__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_end, int vis,
+__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int vis,
                                              int grp, const bf16x8 (&qh)[2],
                                              const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
                                              float& l_run) {
@@ -131,7 +134,7 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int key = blk + grp * 8 + tt * 4 + i;
-      sv[tt * 4 + i] = (!MASKED || (key < k_end && key < vis)) ? st[i] : -INFINITY;
+      sv[tt * 4 + i] = (!MASKED || (key >= k_lo && key < k_end && key < vis)) ? st[i] : -INFINITY;
     }
   }
   const float bm = rows4_max(fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
@@ -225,7 +228,9 @@ attn_mfma_kernel(AttnArgs a) {
   const int q0 = qg * 16;
   const int nq = min(16, s.k + 1 - q0);
   if (nq <= 0) return;
-  const int n_keys = CROSS ? s.T : s.n + q0 + nq;
+  // cross-attention sees frames [wlo, whi) (all frames unless a window was given)
+  const int n_keys = CROSS ? s.whi : s.n + q0 + nq;
+  const int k_lo = CROSS ? s.wlo : 0;
   const int n_chunks = (n_keys + a.chunk - 1) / a.chunk;
   const int ch = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63, c16 = lane & 15, grp = lane >> 4;
@@ -236,8 +241,10 @@ attn_mfma_kernel(AttnArgs a) {
   // a wave past the last chunk issues the loads of chunk 0 (valid addresses, results
   // unused): every wave runs the same straight-line prologue, so the compiler keeps
   // exact outstanding-load counts through it
-  const int k_beg = active ? ch * a.chunk : 0;
-  const int k_end = min(k_beg + a.chunk, n_keys);
+  // the chunk's keys [k_beg, k_end); blocks before the window's first 32-key block are
+  // skipped (a chunk wholly before the window streams nothing and merges with weight 0)
+  const int k_end = min((active ? ch * a.chunk : 0) + a.chunk, n_keys);
+  const int k_beg = max(active ? ch * a.chunk : 0, k_lo / kCrossBlock * kCrossBlock);
   // self-attention: the chunk's page indices, one per lane (lanes past the chunk repeat
   // its first page)
   int pg_lane = 0;
@@ -372,13 +379,13 @@ attn_mfma_kernel(AttnArgs a) {
       // hold committed keys only
       const int clean = CROSS ? k_end : min(k_end, s.n);
       auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
-        if (blk + 32 <= clean) {
-          attend_block<false>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+        if (blk + 32 <= clean && blk >= k_lo) {
+          attend_block<false>(t, blk, k_lo, k_end, vis, grp, qh, ql, o, m_run, l_run);
         } else if (CROSS) {
-          attend_block<true>(t, blk, k_end, vis, grp, qh, ql, o, m_run, l_run);
+          attend_block<true>(t, blk, k_lo, k_end, vis, grp, qh, ql, o, m_run, l_run);
         } else {
-          attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_end, vis,
-                             grp, qh, ql, o, m_run, l_run);
+          attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
+                             vis, grp, qh, ql, o, m_run, l_run);
         }
       };
       for (int blk = k_beg; blk < k_end; blk += 64) {

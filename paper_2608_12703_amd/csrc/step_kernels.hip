@@ -23,6 +23,12 @@ __global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
     }
     if (T < 1 || T > a.max_frames || off < 0 || (off % kCrossBlock) || off + T > a.frames_cap)
       e |= 8;
+    int wlo = 0, whi = T;
+    if (a.cross_window) {
+      wlo = a.cross_window[2 * b];
+      whi = a.cross_window[2 * b + 1];
+      if (wlo < 0 || whi > T || wlo >= whi) e |= 8;
+    }
     if (!(e & 1)) {
       const int last_page = (n + kb) / kTile;
       if (last_page >= a.pages_per_seq) {
@@ -40,7 +46,8 @@ __global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
     }
     if (e) atomicOr(err, e);
     if (e & 1) row0 = 0;
-    seqs[b] = SeqDesc{row0, e ? 0 : kb, e ? 0 : n, e ? 1 : T, e ? 0 : off, e == 0, 0, 0};
+    seqs[b] = SeqDesc{row0, e ? 0 : kb, e ? 0 : n, e ? 1 : T, e ? 0 : off, e == 0, e ? 0 : wlo,
+                      e ? 1 : whi};
   }
 }
 
@@ -78,11 +85,12 @@ __global__ void prep_row_kernel(StepArgs a, const SeqDesc* seqs, RowDesc* rows) 
 
 template <class S>
 __global__ void embed_kernel(int d, const RowDesc* rows, const typename S::T* tok_emb,
-                             const typename S::T* pos_emb, float* x) {
+                             const typename S::T* pos_emb, float* x, const float* in_rows) {
   const int m = blockIdx.x;
   const RowDesc r = rows[m];
   for (int j = threadIdx.x; j < d; j += blockDim.x)
-    x[(size_t)m * d + j] = S::ld(tok_emb, (size_t)r.token * d + j) + S::ld(pos_emb, (size_t)r.pos * d + j);
+    x[(size_t)m * d + j] = (in_rows ? in_rows[(size_t)m * d + j] : S::ld(tok_emb, (size_t)r.token * d + j)) +
+                           S::ld(pos_emb, (size_t)r.pos * d + j);
 }
 
 // ---------------------------------------------------------------- LayerNorm
@@ -249,6 +257,7 @@ template <class S>
 __global__ void __launch_bounds__(256) embed_ln_kernel(int d, const RowDesc* rows,
                                                        const typename S::T* tok_emb,
                                                        const typename S::T* pos_emb, float* x,
+                                                       const float* in_rows,
                                                        const typename S::T* g,
                                                        const typename S::T* b, uint16_t* frag,
                                                        int RT) {
@@ -258,7 +267,8 @@ __global__ void __launch_bounds__(256) embed_ln_kernel(int d, const RowDesc* row
   const RowDesc r = rows[m];
   float sum = 0.f;
   for (int j = threadIdx.x; j < d; j += 256) {
-    const float v = S::ld(tok_emb, (size_t)r.token * d + j) + S::ld(pos_emb, (size_t)r.pos * d + j);
+    const float v = (in_rows ? in_rows[(size_t)m * d + j] : S::ld(tok_emb, (size_t)r.token * d + j)) +
+                    S::ld(pos_emb, (size_t)r.pos * d + j);
     x[(size_t)m * d + j] = v;
     row[j] = v;
     sum += v;
@@ -419,12 +429,12 @@ void launch_prep(const StepArgs& a, SeqDesc* seqs, RowDesc* rows, int* err, hipS
 
 template <class S>
 void launch_embed(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
-                  hipStream_t st) {
+                  const float* in_rows, hipStream_t st) {
   hipLaunchKernelGGL(embed_kernel<S>, dim3(M), dim3(256), 0, st, d, rows,
-                     (const typename S::T*)tok, (const typename S::T*)pos, x);
+                     (const typename S::T*)tok, (const typename S::T*)pos, x, in_rows);
 }
-template void launch_embed<F32>(int, int, const RowDesc*, const void*, const void*, float*, hipStream_t);
-template void launch_embed<BF16>(int, int, const RowDesc*, const void*, const void*, float*, hipStream_t);
+template void launch_embed<F32>(int, int, const RowDesc*, const void*, const void*, float*, const float*, hipStream_t);
+template void launch_embed<BF16>(int, int, const RowDesc*, const void*, const void*, float*, const float*, hipStream_t);
 
 template <class S>
 void launch_layernorm(int M, int d, const float* x, const void* g, const void* b, float* out,
@@ -452,10 +462,76 @@ void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* 
 }
 
 void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
-                     const void* g, const void* b, uint16_t* frag, int RT, hipStream_t st) {
+                     const float* in_rows, const void* g, const void* b, uint16_t* frag, int RT,
+                     hipStream_t st) {
   hipLaunchKernelGGL(embed_ln_kernel<BF16>, dim3(M), dim3(256), d * sizeof(float), st, d, rows,
-                     (const uint16_t*)tok, (const uint16_t*)pos, x, (const uint16_t*)g,
+                     (const uint16_t*)tok, (const uint16_t*)pos, x, in_rows, (const uint16_t*)g,
                      (const uint16_t*)b, frag, RT);
+}
+
+// ---------------------------------------------------------------- draft-block inputs
+
+// taps4[b] = [taps_0 ; taps_1 ; taps_2 ; hidden] at sequence b's last verified row (zeros
+// for a skipped sequence).
+__global__ void draft_gather_taps_kernel(int d, int layout, int k_max, const int* cu_rows,
+                                         const int* accept_len, int rows, const float* taps,
+                                         const float* hidden, float* taps4) {
+  const int b = blockIdx.x;
+  const int a = accept_len[b];
+  const int row = (layout == 0 ? b * (k_max + 1) : cu_rows[b]) + (a < 0 ? 0 : a);
+  for (int j = threadIdx.x; j < 4 * d; j += blockDim.x) {
+    const int which = j / d, c = j % d;
+    const float* src = which < 3 ? taps + ((size_t)which * rows + row) * d : hidden + (size_t)row * d;
+    taps4[(size_t)b * 4 * d + j] = a < 0 ? 0.f : src[c];
+  }
+}
+
+// z[b] = [feat[b] ; E_tok[token_b]], token_b = tokens[b * token_stride + (token_index ?
+// token_index[b] : 0)] (a negative index, i.e. a skipped sequence, reads slot 0).
+template <class S>
+__global__ void draft_concat_kernel(int d, const float* feat, const typename S::T* tok_emb,
+                                    const int* tokens, int token_stride, const int* token_index,
+                                    float* z) {
+  const int b = blockIdx.x;
+  const int ti = token_index ? max(token_index[b], 0) : 0;
+  const int t = max(tokens[(size_t)b * token_stride + ti], 0);
+  for (int j = threadIdx.x; j < 2 * d; j += blockDim.x)
+    z[(size_t)b * 2 * d + j] = j < d ? feat[(size_t)b * d + j] : S::ld(tok_emb, (size_t)t * d + (j - d));
+}
+
+// window[b] = [max(0, c - half), min(T_b, c + half + 1)) around anchor c (a negative
+// anchor, i.e. a skipped sequence, gives the first frame).
+__global__ void draft_window_kernel(int B, const int* anchor, const int* enc_len, int half, int* window) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int c = max(anchor[b], 0), T = max(enc_len[b], 1);
+  const int lo = max(0, min(c - half, T - 1));
+  window[2 * b] = lo;
+  window[2 * b + 1] = max(lo + 1, min(T, c + half + 1));
+}
+
+void launch_draft_gather_taps(int B, int d, int layout, int k_max, const int* cu_rows,
+                              const int* accept_len, int rows, const float* taps,
+                              const float* hidden, float* taps4, hipStream_t st) {
+  hipLaunchKernelGGL(draft_gather_taps_kernel, dim3(B), dim3(256), 0, st, d, layout, k_max, cu_rows,
+                     accept_len, rows, taps, hidden, taps4);
+}
+
+void launch_draft_concat(int B, int d, const float* feat, const void* tok_emb, int bf16,
+                         const int* tokens, int token_stride, const int* token_index, float* z,
+                         hipStream_t st) {
+  if (bf16)
+    hipLaunchKernelGGL(draft_concat_kernel<BF16>, dim3(B), dim3(256), 0, st, d, feat,
+                       (const uint16_t*)tok_emb, tokens, token_stride, token_index, z);
+  else
+    hipLaunchKernelGGL(draft_concat_kernel<F32>, dim3(B), dim3(256), 0, st, d, feat,
+                       (const float*)tok_emb, tokens, token_stride, token_index, z);
+}
+
+void launch_draft_window(int B, const int* anchor, const int* enc_len, int half, int* window,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(draft_window_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, anchor,
+                     enc_len, half, window);
 }
 
 void launch_zero_i32(int* p, int n, hipStream_t st) {

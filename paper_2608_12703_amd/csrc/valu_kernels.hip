@@ -131,10 +131,12 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
       const int r = i >> 6, j = i & 63;
       qs[r][j] = r < nq ? q[(size_t)(s.row0 + qg + r) * d + h * kHead + j] : 0.f;
     }
-    const int vis = CROSS ? s.T : s.n + qg + qi + 1;
-    const int n_keys = CROSS ? s.T : s.n + qg + nq;
+    // cross-attention sees frames [wlo, whi) (all frames unless a window was given)
+    const int lo = CROSS ? s.wlo : 0;
+    const int vis = CROSS ? s.whi : s.n + qg + qi + 1;
+    const int n_keys = CROSS ? s.whi : s.n + qg + nq;
     float m_run = -INFINITY, l_run = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < n_keys; c0 += 64) {
+    for (int c0 = lo / 64 * 64; c0 < n_keys; c0 += 64) {
       __syncthreads();
       for (int i = tid; i < 64 * 64; i += 256) {
         const int key = i >> 6, j = i & 63, t = c0 + key;
@@ -164,7 +166,7 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
         float acc = 0.f;
 #pragma unroll 16
         for (int j = 0; j < 64; ++j) acc = fmaf(qs[qi][j], ks[key][j], acc);
-        sc[u] = (c0 + key < vis && qi < nq) ? acc * 0.125f : -INFINITY;
+        sc[u] = (c0 + key >= lo && c0 + key < vis && qi < nq) ? acc * 0.125f : -INFINITY;
       }
       float cm = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
 #pragma unroll

@@ -97,3 +97,108 @@ def decode_with_drift(sess, ys, plans, k: int, n_tokens: int):
         if int(n.max()) >= MAX_POS:
             break
     return [t[:n_tokens] for t in toks], accepts, rounds
+
+
+# ---------------------------------------------------------------------- audio-conditioned draft
+
+HALF_WINDOW = 20   # frames: +-400 ms at 20 ms per encoder frame
+
+
+class DraftRunner:
+    """The audio-conditioned draft block of a target session: a one-layer model of the
+    target's form (its own block and final LayerNorm, the target's token and position
+    tables) run through ad_verify_step with one row per sequence, fed by ad_draft_input.
+
+    Rounds start from a target step that was run with anchor_layer >= 0 and three
+    tap_layers (see Session); every draft step is a device-side pair of calls.
+    """
+
+    def __init__(self, target, draft_params: dict, pack_weights: bool = True):
+        from .harness import Session, upload
+        cfg, B = target.cfg, target.B
+        self.target, self.B = target, B
+        self.dcfg = synth.draft_config(cfg)
+        dt = target.dt
+        dev = target.device
+        own = {n: upload(draft_params[n], dt, dev) for n, _ in synth.draft_param_specs(cfg)}
+        shared = {"tok_emb": target.params[0], "pos_emb": target.params[1]}
+        plist = [shared[n] if n in shared else own[n] for n, _ in synth.param_specs(self.dcfg)]
+        self.sess = Session(self.dcfg, plist, B, 0, target.frames, page_seed=None,
+                            pack_weights=pack_weights, device=dev)
+        self.fuse = [own[n] for n in synth.DRAFT_EXTRA]
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.tokens = torch.zeros(B, **i32)
+        self.sess.in_rows = torch.zeros(B, cfg.d_model, dtype=torch.float32, device=dev)
+        self.sess.cross_window = torch.zeros(B, 2, **i32)
+        self.ws = torch.empty(ad.draft_input_workspace_size(target.model, B), dtype=torch.uint8,
+                              device=dev)
+        self.sess.prepare([np.zeros(1, np.int64)] * B)
+        self.sess.step_struct.tokens = self.tokens.data_ptr()
+
+    def prefill_encoder(self, encs):
+        """The draft's own cross-attention keys / values of the encoder states."""
+        self.sess.prefill_encoder(encs)
+
+    def _input(self, first: bool):
+        t, s = self.target, self.sess
+        if first:
+            ad.draft_input(t.model, *self.fuse, self.B, t.out_taps, t.out_hidden, t.cur_layout,
+                           t.k_max, t.cu_rows, t.accept_len, t.rows, None, t.out_tokens,
+                           t.k_max + 1, t.accept_len, t.out_anchor, s.enc_len, HALF_WINDOW,
+                           s.cross_window, s.in_rows, self.ws)
+        else:
+            ad.draft_input(t.model, *self.fuse, self.B, None, None, t.cur_layout, t.k_max,
+                           None, None, t.rows, s.out_hidden, s.out_greedy, 1, None, None, None,
+                           0, None, s.in_rows, self.ws)
+
+    def round(self, K: int, out=None):
+        """K draft steps after the target step last run; returns a device [B, K] int32
+        tensor of drafts (the tokens fed are the pending token, then each draft)."""
+        s = self.sess
+        out = torch.empty(self.B, K, dtype=torch.int32, device=s.device) if out is None else out
+        s.kv_len.zero_()
+        # the step's token ids are only validated and scanned (k = 0): its input is in_rows,
+        # built by ad_draft_input from the real tokens (the pending token, then each draft)
+        self.tokens.zero_()
+        for j in range(K):
+            self._input(first=j == 0)
+            s.run()
+            s.commit()
+            out[:, j].copy_(s.out_greedy[: self.B])
+            self.tokens.copy_(s.out_greedy[: self.B])
+        return out
+
+
+def decode_with_draft(target, runner: DraftRunner, t0, K: int, n_tokens: int, anchor_layer: int):
+    """Greedy speculative decode with the audio-conditioned draft: every round verifies
+    [pending, d_1..d_k] on the target (with the anchor readout and the draft's taps),
+    commits, and drafts the next block.  Round 0 verifies the pending token alone.
+    Returns (tokens [B][n_tokens], accepts, drafts, rounds)."""
+    B = target.B
+    L = target.cfg.n_layers
+    target.anchor_layer = anchor_layer
+    target.tap_layers = tuple(max(0, L * i // 4 - 1) for i in (1, 2, 3))
+    target.out_taps = torch.empty(3, target.max_rows, target.cfg.d_model, dtype=torch.float32,
+                                  device=target.device)
+    toks = [[] for _ in range(B)]
+    accepts, drafts = [], []
+    n = target.kv_len.cpu().numpy().astype(np.int64)
+    blocks = [np.array([int(t0[b])], np.int64) for b in range(B)]
+    rounds = 0
+    while min(len(t) for t in toks) < n_tokens:
+        drafts.append([blk[1:].copy() for blk in blocks])
+        target.step(blocks)
+        target.commit()
+        nxt = runner.round(K).cpu().numpy()
+        res = target.results()
+        assert res["err"] == 0, f"device error flag {res['err']}"
+        a = res["accept_len"]
+        accepts.append(a.copy())
+        for b in range(B):
+            emitted = [int(x) for x in res["out_tokens"][b][: a[b] + 1]]
+            toks[b] += emitted
+            n[b] += a[b] + 1
+            k = _clamp_k(K, int(n[b]))
+            blocks[b] = np.concatenate([[emitted[-1]], nxt[b][:k]]).astype(np.int64)
+        rounds += 1
+    return [t[:n_tokens] for t in toks], accepts, drafts, rounds

@@ -6,6 +6,8 @@ outputs, and the workspace.  It only moves data and calls libad entry points.
 """
 from __future__ import annotations
 
+import ctypes
+
 import numpy as np
 import torch
 
@@ -86,6 +88,12 @@ class Session:
         self.anchor_layer = -1
         self.out_anchor = torch.full((batch,), -1, **i32)
         self.out_anchor_peak = torch.zeros(batch, dtype=torch.float32, device=device)
+        # draft-block use: input rows replacing the token embedding, a per-sequence
+        # cross-attention window, and residual taps (tap_layers -1: none)
+        self.in_rows = None
+        self.cross_window = None
+        self.tap_layers = (-1, -1, -1)
+        self.out_taps = None
         self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch, k_max),
                                      dtype=torch.uint8, device=device)
         self.step_struct = None
@@ -152,7 +160,8 @@ class Session:
             self.out_tokens.data_ptr(), self.out_greedy.data_ptr(), ad.ptr(self.out_logits),
             self.out_hidden.data_ptr(), self.out_margin.data_ptr(), self.err_flag.data_ptr(),
             self.workspace.data_ptr(), self.workspace.numel(), int(self.anchor_layer),
-            self.out_anchor.data_ptr(), self.out_anchor_peak.data_ptr())
+            self.out_anchor.data_ptr(), self.out_anchor_peak.data_ptr(), ad.ptr(self.in_rows),
+            ad.ptr(self.cross_window), (ctypes.c_int32 * 3)(*self.tap_layers), ad.ptr(self.out_taps))
         self.cur_layout = layout
         return self.step_struct
 

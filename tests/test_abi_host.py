@@ -82,7 +82,8 @@ def _step(ad, **over):
     kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
     cross = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
     s = ad.Step(2, ad.AD_PADDED, 3, 8, 0x1000, 0x1000, None, kv, cross, 0x1000, 0x1000, None, None,
-                None, None, 0x1000, 0x1000, 1 << 40, -1, None, None)
+                None, None, 0x1000, 0x1000, 1 << 40, -1, None, None, None, None,
+                (ctypes.c_int32 * 3)(-1, -1, -1), None)
     for k, v in over.items():
         setattr(s, k, v)
     return s
@@ -107,6 +108,23 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert run(_step(ad, anchor_layer=-2)) == -2
     assert run(_step(ad, anchor_layer=cfg.n_layers)) == -2
     assert run(_step(ad, anchor_layer=0)) == -1                     # readout without out_anchor
+    assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(-1, -1, cfg.n_layers))) == -2
+    assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(0, -1, -1))) == -1   # taps without out_taps
+    ws = ctypes.c_size_t()
+    assert ad.LIB.ad_draft_input_workspace_size(h, 2, ctypes.byref(ws)) == 0
+    assert ws.value == 7 * cfg.d_model * 2 * 4
+    di = lambda **o: ad.LIB.ad_draft_input(
+        h, o.get("w_fuse", 0x1000), 0x1000, 0x1000, 0x1000, o.get("batch", 2), o.get("taps", 0x1000),
+        0x1000, o.get("layout", ad.AD_PADDED), 3, None, 0x1000, o.get("rows", 8), None, 0x1000,
+        o.get("stride", 4), 0x1000, o.get("anchor", None), 0x1000, o.get("half", 20), 0x1000,
+        0x1000, 0x1000, o.get("ws", ws.value), None)
+    assert di(w_fuse=None) == -1
+    assert di(layout=7) == -1
+    assert di(layout=ad.AD_PACKED) == -1                            # packed without cu_rows
+    assert di(taps=None) == -1                                      # neither taps nor feature
+    assert di(batch=0) == -2 and di(stride=0) == -2 and di(rows=1) == -2
+    assert di(anchor=0x1000, half=-1) == -2
+    assert di(ws=ws.value - 1) == -3
     assert run(_step(ad, workspace_bytes=100)) == -3
     assert b"workspace" in ad.LIB.ad_last_error()
     assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1

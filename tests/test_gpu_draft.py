@@ -1,0 +1,140 @@
+"""GPU parity of the audio-conditioned draft step against the oracle.
+
+Paper, section 3 "Models and Protocol" and appendix "Draft architecture" (EAGLE-3-style
+draft from four target representations and the token embedding, one causal block with
+audio cross-attention), appendix "Window geometry" (+-400 ms around the anchor).  The
+target step runs with the verification-attention anchor readout and three residual
+taps; the draft round's every input on the oracle side comes from the oracle's own
+target pass.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from oracle import draft as odr
+from paper_2608_12703_amd import ad, decode, synth
+from paper_2608_12703_amd.configs import Config
+from paper_2608_12703_amd.harness import Session
+
+from gpu_common import MARGIN_EXCLUDE, device_session, oracle_model, oracle_state, planted_blocks
+
+pytestmark = pytest.mark.gpu
+
+UNIT = Config(name="unit_draft", n_layers=3, d_model=128, n_heads=2, d_ffn=256, vocab=1000,
+              dtype="bf16", batch=4, k=4, k_min=0, frames=300, frames_min=40, kv_max=60,
+              geo_p=0.3, seed=5)
+ANCHOR_LAYER, K = 1, 5
+
+
+def _target_step(cfg, params, wl, blocks):
+    sess = device_session(cfg, params, wl)
+    sess.anchor_layer = ANCHOR_LAYER
+    sess.tap_layers = tuple(odr.tap_layers(cfg.n_layers))
+    sess.out_taps = torch.empty(3, sess.max_rows, cfg.d_model, dtype=torch.float32, device="cuda")
+    sess.step(blocks)
+    return sess
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_draft_round_matches_oracle(dtype):
+    cfg = UNIT.with_(dtype=dtype)
+    params = synth.make_params(cfg)
+    dparams = synth.make_draft_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, set(range(wl.batch)))
+    sess = _target_step(cfg, params, wl, blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    runner = decode.DraftRunner(sess, dparams)
+    runner.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+    got = runner.round(K).cpu().numpy()
+    feat = runner.sess.out_hidden[: wl.batch].cpu().numpy()
+    bm = odr.block_model(synth.draft_config(cfg), params, dparams)
+    compared = 0
+    for b in range(wl.batch):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref, anc = od.verify_with_anchor(model, st, blocks[b][1:], ANCHOR_LAYER)
+        a = ref.accepted
+        if int(res["accept_len"][b]) != a or int(res["anchor"][b]) != anc.frame:
+            print(f"  seq {b}: target decision differs (near tie), draft not compared")
+            continue
+        out = od.forward_block(model, st, blocks[b], taps=odr.tap_layers(cfg.n_layers))
+        dcross = od.cross_kv(bm, synth.make_encoder(cfg, b, int(wl.T[b])))
+        want = odr.draft_round(bm, dparams, dcross, out.taps[:, a], out.hidden[a], ref.greedy[a],
+                               anc.frame, int(wl.T[b]), K)
+        cut = next((j for j, m in enumerate(want.margins) if m < MARGIN_EXCLUDE), K)
+        print(f"  seq {b}: a={a} anchor={anc.frame} drafts gpu {got[b].tolist()} oracle {want.drafts} "
+              f"(compared {cut}), margins {np.round(want.margins, 4).tolist()}")
+        assert got[b][:cut].tolist() == want.drafts[:cut]
+        if cut == K:   # the last step's output feature
+            err = np.max(np.abs(feat[b] - want.hidden[-1]))
+            assert err < (2e-2 if dtype == "bf16" else 1e-4), f"seq {b}: feature error {err}"
+        compared += 1
+    assert compared >= wl.batch - 1
+
+
+def test_draft_sees_only_its_window():
+    cfg = UNIT
+    params = synth.make_params(cfg)
+    dparams = synth.make_draft_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    blocks = [np.concatenate([[wl.t0[b]], wl.fill_any[b]]) for b in range(wl.batch)]
+    sess = _target_step(cfg, params, wl, blocks)
+    anchors = sess.results()["anchor"]
+    encs = [synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)]
+    runner = decode.DraftRunner(sess, dparams)
+    runner.prefill_encoder(encs)
+    d1 = runner.round(K).cpu().numpy()
+    f1 = runner.sess.out_hidden[: wl.batch].cpu().numpy()
+    # audio outside each sequence's window replaced: the round must not change at all
+    encs2 = []
+    for b, e in enumerate(encs):
+        lo, hi = odr.window(int(anchors[b]), int(wl.T[b]))
+        e2 = np.full_like(e, 7.0)
+        e2[lo:hi] = e[lo:hi]
+        encs2.append(e2)
+    runner.prefill_encoder(encs2)
+    d2 = runner.round(K).cpu().numpy()
+    f2 = runner.sess.out_hidden[: wl.batch].cpu().numpy()
+    np.testing.assert_array_equal(d1, d2)
+    np.testing.assert_array_equal(f1.view(np.uint32), f2.view(np.uint32))
+    # and the window matters: all-new audio changes the features
+    runner.prefill_encoder([np.full_like(e, 7.0) for e in encs])
+    runner.round(K)
+    assert not np.array_equal(runner.sess.out_hidden[: wl.batch].cpu().numpy(), f1)
+
+
+def test_speculative_decode_with_draft_equals_autoregressive():
+    cfg = UNIT.with_(kv_max=0)
+    params = synth.make_params(cfg)
+    dparams = synth.make_draft_params(cfg)
+    B, T, n_tokens = 3, 250, 24
+    encs = [synth.make_encoder(cfg, b, T) for b in range(B)]
+
+    def session():
+        s = Session(cfg, params, B, K, [T] * B)
+        s.prefill_encoder(encs)
+        s.set_kv_len(np.zeros(B, np.int64))
+        return s
+
+    # autoregressive reference on the GPU: k = 0 steps
+    ar = session()
+    toks = [[] for _ in range(B)]
+    start = 17                     # a start token inside this test vocabulary
+    pend = [start] * B
+    for _ in range(n_tokens):
+        ar.step([np.array([p], np.int64) for p in pend])
+        ar.commit()
+        r = ar.results()
+        for b in range(B):
+            pend[b] = int(r["out_tokens"][b][0])
+            toks[b].append(pend[b])
+    tgt = session()
+    runner = decode.DraftRunner(tgt, dparams)
+    runner.prefill_encoder(encs)
+    got, acc, drafts, rounds = decode.decode_with_draft(tgt, runner, [start] * B, K, n_tokens,
+                                                         ANCHOR_LAYER)
+    print(f"[draft loop] {rounds} rounds, accepts {[a.tolist() for a in acc]}")
+    assert got == toks
