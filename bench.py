@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--anchor-layer", type=int, default=-2,
                    help="also time the step with the verification-attention anchor readout at "
                         "this layer (-2: three quarters of the depth; -1: skip)")
+    p.add_argument("--draft-steps", type=int, default=6,
+                   help="also time this many audio-conditioned draft steps per round (0: skip)")
     p.add_argument("--copy-calibration-mb", type=int, default=0,
                    help="after the timed steps, copy a buffer of this many MiB once (a plain "
                         "copy of known size that calibrates HBM byte counters)")
@@ -237,6 +239,39 @@ def main():
         sess.anchor_layer = -1
         sess.prepare(blocks)
 
+    draft = None
+    if args.draft_steps > 0:
+        # The audio-conditioned draft block (random-init, one layer, d_ffn = 2 d) after a
+        # target step that also reads the anchor and the draft's taps; rho = one draft
+        # step's time over one verify step's time.
+        from paper_2608_12703_amd import decode
+        K = args.draft_steps
+        L = cfg.n_layers
+        sess.anchor_layer = 3 * L // 4
+        sess.tap_layers = tuple(max(0, L * i // 4 - 1) for i in (1, 2, 3))
+        sess.out_taps = torch.empty(3, sess.max_rows, cfg.d_model, dtype=torch.float32, device="cuda")
+        sess.prepare(blocks)
+        one_step()
+        runner = decode.DraftRunner(sess, synth.make_draft_params(cfg))
+        runner.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+        for _ in range(2):
+            runner.round(K)
+        torch.cuda.synchronize()
+        rounds = max(1, args.steps // 2)
+        ev0.record(stream)
+        for _ in range(rounds):
+            runner.round(K)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        us = ev0.elapsed_time(ev1) / (rounds * K) * 1e3
+        draft = {"draft_steps_per_round": K, "us_per_draft_step": round(us, 2),
+                 "rho": round(us / (ms * 1e3), 4), "layers": 1, "d_ffn": 2 * cfg.d_model,
+                 "cross_window_frames": 2 * decode.HALF_WINDOW + 1}
+        log(f"draft step: {us:.1f} us (rho = {us / (ms * 1e3):.4f})")
+        sess.anchor_layer, sess.tap_layers, sess.out_taps = -1, (-1, -1, -1), None
+        sess.prepare(blocks)
+        del runner
+
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
@@ -269,6 +304,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "anchor_readout": anchor,
+        "draft_step": draft,
     }
     print(json.dumps(out), flush=True)
 

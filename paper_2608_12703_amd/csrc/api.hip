@@ -552,10 +552,35 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   return check_hip("ad_verify_step");
 }
 
+// ad_draft_input's scratch.  float32 models: the gathered rows [B][4d], the feature
+// [B][d] and the concatenated rows [B][2d] for the VALU products.  bf16 models: the
+// matrix-core products' A operand (A-fragment order, up to 4d wide), their split-K
+// partials and the feature.
+struct DraftInputWs {
+  size_t frag, part, feat, bytes;
+  int RT;
+};
+DraftInputWs draft_input_ws(const ad_model_desc& D, int B) {
+  DraftInputWs w{};
+  const size_t d = D.d_model;
+  if (D.dtype != AD_BF16) {
+    w.bytes = sizeof(float) * 7 * d * B;
+    return w;
+  }
+  w.RT = div_up(div_up(B, 16), 16) * 16;
+  w.frag = 0;
+  w.part = align256((size_t)w.RT * 16 * 4 * d * 4);
+  const size_t parts = std::max(ad::gemm_part_floats(B, (int)d, 4 * (int)d),
+                                ad::gemm_part_floats(B, (int)d, 2 * (int)d));
+  w.feat = w.part + align256(4 * parts);
+  w.bytes = w.feat + align256(4 * d * B);
+  return w;
+}
+
 ad_status ad_draft_input_workspace_size(const ad_model* model, int32_t batch, size_t* bytes) {
   if (!model || !bytes) return fail(AD_EINVAL, "NULL argument");
   if (batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
-  *bytes = sizeof(float) * 7 * (size_t)model->desc.d_model * batch;
+  *bytes = draft_input_ws(model->desc, batch).bytes;
   return AD_OK;
 }
 
@@ -587,13 +612,41 @@ ad_status ad_draft_input(const ad_model* model, const void* w_fuse, const void* 
   if (workspace_bytes < need) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need) + " bytes");
   (void)hipGetLastError();
   hipStream_t st = (hipStream_t)stream;
+  if (D.dtype == AD_BF16) {
+    // matrix-core products: A operand in fragment order, split-K partials, then the sum
+    // of the partials plus the bias
+    const DraftInputWs w = draft_input_ws(D, batch);
+    char* base = (char*)workspace;
+    uint16_t* frag = (uint16_t*)(base + w.frag);
+    float* part = (float*)(base + w.part);
+    float* feat = (float*)(base + w.feat);
+    auto product = [&](int K, const void* W, const void* bias, float* dst) {
+      ad::GemmArgs g{};
+      g.M = batch; g.N = d; g.K = K; g.RT = w.RT; g.A = frag; g.W = (const uint16_t*)W;
+      g.packed = 0; g.part = part;
+      ad::launch_gemm_mfma(ad::EPI_PARTIAL, g, st);
+      ad::launch_sum_partials_bias(batch, d, ad::gemm_splits(d, K), part, bias, dst, st);
+    };
+    const float* f = feature;
+    if (taps) {
+      ad::launch_draft_gather_taps_frag(batch, d, layout, k_max, cu_rows, accept_len, rows, taps,
+                                        hidden, frag, w.RT, st);
+      product(4 * d, w_fuse, b_fuse, feat);
+      f = feat;
+    }
+    ad::launch_draft_concat_frag(batch, d, f, model->p[P_TOK], tokens, token_stride, token_index,
+                                 frag, w.RT, st);
+    product(2 * d, w_in, b_in, out);
+    if (anchor) ad::launch_draft_window(batch, anchor, enc_len, half_window, window, st);
+    return check_hip("ad_draft_input");
+  }
   float* taps4 = (float*)workspace;
   float* feat = taps4 + (size_t)4 * d * batch;
   float* z = feat + (size_t)d * batch;
   const float* f = feature;
   ad::EpiArgs e{};
   e.ldo = d;
-  const bool bf16 = D.dtype == AD_BF16;
+  const bool bf16 = false;
   if (taps) {
     ad::launch_draft_gather_taps(batch, d, layout, k_max, cu_rows, accept_len, rows, taps, hidden,
                                  taps4, st);

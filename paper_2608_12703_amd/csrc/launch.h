@@ -178,6 +178,17 @@ void launch_draft_concat(int B, int d, const float* feat, const void* tok_emb, i
                          hipStream_t st);
 void launch_draft_window(int B, const int* anchor, const int* enc_len, int half, int* window,
                          hipStream_t st);
+// The same inputs for the matrix-core product: written in A-fragment order (RT row tiles)
+// instead of float32 rows.
+void launch_draft_gather_taps_frag(int B, int d, int layout, int k_max, const int* cu_rows,
+                                   const int* accept_len, int rows, const float* taps,
+                                   const float* hidden, uint16_t* frag, int RT, hipStream_t st);
+void launch_draft_concat_frag(int B, int d, const float* feat, const void* tok_emb,
+                              const int* tokens, int token_stride, const int* token_index,
+                              uint16_t* frag, int RT, hipStream_t st);
+// out[m][n] = sum_s P[s][m][n] (split order) + bias[n], float32 rows.
+void launch_sum_partials_bias(int M, int N, int nsplit, const float* P, const void* bias, float* out,
+                              hipStream_t st);
 
 // Attention of every block row over the paged self cache (causal inside the block) or
 // over the sequence's encoder frames.  q and out are float32 [rows][d].

@@ -510,6 +510,61 @@ __global__ void draft_window_kernel(int B, const int* anchor, const int* enc_len
   window[2 * b + 1] = max(lo + 1, min(T, c + half + 1));
 }
 
+__global__ void draft_gather_taps_frag_kernel(int d, int layout, int k_max, const int* cu_rows,
+                                              const int* accept_len, int rows, const float* taps,
+                                              const float* hidden, uint16_t* frag, int RT) {
+  const int b = blockIdx.x;
+  const int a = accept_len[b];
+  const int row = (layout == 0 ? b * (k_max + 1) : cu_rows[b]) + (a < 0 ? 0 : a);
+  for (int j = threadIdx.x; j < 4 * d; j += blockDim.x) {
+    const int which = j / d, c = j % d;
+    const float* src = which < 3 ? taps + ((size_t)which * rows + row) * d : hidden + (size_t)row * d;
+    afrag_store(frag, RT, b, j, a < 0 ? 0.f : src[c]);
+  }
+}
+
+__global__ void draft_concat_frag_kernel(int d, const float* feat, const uint16_t* tok_emb,
+                                         const int* tokens, int token_stride, const int* token_index,
+                                         uint16_t* frag, int RT) {
+  const int b = blockIdx.x;
+  const int ti = token_index ? max(token_index[b], 0) : 0;
+  const int t = max(tokens[(size_t)b * token_stride + ti], 0);
+  for (int j = threadIdx.x; j < 2 * d; j += blockDim.x)
+    afrag_store(frag, RT, b, j, j < d ? feat[(size_t)b * d + j] : bf16_to_f32(tok_emb[(size_t)t * d + (j - d)]));
+}
+
+__global__ void sum_partials_bias_kernel(int M, int N, int nsplit, const float* P,
+                                         const uint16_t* bias, float* out) {
+  const int m = blockIdx.x;
+  for (int j = threadIdx.x * 4; j < N; j += blockDim.x * 4) {
+    const size_t e = (size_t)m * N + j;
+    float4 v = split_sum4_flat(P, (size_t)M * N, e, nsplit);
+    const float4 bb = ld_bf16x4(bias, j);
+    v.x += bb.x; v.y += bb.y; v.z += bb.z; v.w += bb.w;
+    *(float4*)(out + e) = v;
+  }
+}
+
+void launch_draft_gather_taps_frag(int B, int d, int layout, int k_max, const int* cu_rows,
+                                   const int* accept_len, int rows, const float* taps,
+                                   const float* hidden, uint16_t* frag, int RT, hipStream_t st) {
+  hipLaunchKernelGGL(draft_gather_taps_frag_kernel, dim3(B), dim3(256), 0, st, d, layout, k_max,
+                     cu_rows, accept_len, rows, taps, hidden, frag, RT);
+}
+
+void launch_draft_concat_frag(int B, int d, const float* feat, const void* tok_emb,
+                              const int* tokens, int token_stride, const int* token_index,
+                              uint16_t* frag, int RT, hipStream_t st) {
+  hipLaunchKernelGGL(draft_concat_frag_kernel, dim3(B), dim3(256), 0, st, d, feat,
+                     (const uint16_t*)tok_emb, tokens, token_stride, token_index, frag, RT);
+}
+
+void launch_sum_partials_bias(int M, int N, int nsplit, const float* P, const void* bias, float* out,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(sum_partials_bias_kernel, dim3(M), dim3(256), 0, st, M, N, nsplit, P,
+                     (const uint16_t*)bias, out);
+}
+
 void launch_draft_gather_taps(int B, int d, int layout, int k_max, const int* cu_rows,
                               const int* accept_len, int rows, const float* taps,
                               const float* hidden, float* taps4, hipStream_t st) {

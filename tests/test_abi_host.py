@@ -112,7 +112,7 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(0, -1, -1))) == -1   # taps without out_taps
     ws = ctypes.c_size_t()
     assert ad.LIB.ad_draft_input_workspace_size(h, 2, ctypes.byref(ws)) == 0
-    assert ws.value == 7 * cfg.d_model * 2 * 4
+    assert ws.value >= 7 * cfg.d_model * 2 * 4
     di = lambda **o: ad.LIB.ad_draft_input(
         h, o.get("w_fuse", 0x1000), 0x1000, 0x1000, 0x1000, o.get("batch", 2), o.get("taps", 0x1000),
         0x1000, o.get("layout", ad.AD_PADDED), 3, None, 0x1000, o.get("rows", 8), None, 0x1000,
