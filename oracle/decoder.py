@@ -55,14 +55,15 @@ def softmax(s):
 def attention(q, K, V, visible):
     """Multi-head attention for a few query rows.
 
-    q: [r, H, 64]; K, V: [n_keys, H, 64]; row i sees keys 0..visible[i]-1.
+    q: [r, H, 64]; K, V: [n_keys, H, 64]; row i sees keys 0..visible[i]-1, or, when
+    visible[i] is a boolean array over the keys, the keys it marks.
     Returns [r, H, 64].
     """
     out = np.empty_like(q)
     for i in range(q.shape[0]):
-        nv = int(visible[i])
-        s = np.einsum("hd,thd->ht", q[i], K[:nv]) / np.sqrt(HEAD)
-        out[i] = np.einsum("ht,thd->hd", softmax(s), V[:nv])
+        sel = np.arange(int(visible[i])) if np.ndim(visible[i]) == 0 else np.flatnonzero(visible[i])
+        s = np.einsum("hd,thd->ht", q[i], K[sel]) / np.sqrt(HEAD)
+        out[i] = np.einsum("ht,thd->hd", softmax(s), V[sel])
     return out
 
 
@@ -150,20 +151,47 @@ class BlockOut:
     taps: np.ndarray | None = None    # [n_taps, r, d] residual stream after the tapped layers
 
 
+def tree_depths(parents):
+    """Depth of every node of a draft tree (node 0, the root, has depth 0; parent[i] < i)."""
+    depth = [0] * len(parents)
+    for i in range(1, len(parents)):
+        depth[i] = depth[int(parents[i])] + 1
+    return depth
+
+
+def tree_visibility(parents, n: int):
+    """Keys each block row may attend to in a tree block: the n committed positions and
+    the row's ancestors and itself ([r, n + r] booleans)."""
+    r = len(parents)
+    vis = np.zeros((r, n + r), dtype=bool)
+    vis[:, :n] = True
+    for i in range(r):
+        j = i
+        while True:
+            vis[i, n + j] = True
+            if j == 0:
+                break
+            j = int(parents[j])
+    return vis
+
+
 def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None = None,
-                  in_rows=None, cross_window=None, taps=None) -> BlockOut:
+                  in_rows=None, cross_window=None, taps=None, parents=None) -> BlockOut:
     """One causal decoder pass over ``tokens`` placed at positions n..n+r-1.  With
     ``probe_layer`` set, also returns that layer's cross-attention weights.
 
     in_rows [r, d]: replaces the token embedding of the rows (the position embedding is
     still added).  cross_window (lo, hi): the rows attend to frames lo..hi-1 only.
     taps: list of layer indices; the residual stream after each is returned in
-    ``BlockOut.taps`` [len(taps), r, d]."""
+    ``BlockOut.taps`` [len(taps), r, d].
+    parents: a draft tree over the rows (parents[0] ignored, parents[i] < i): row i
+    sits at position n + depth(i) and attends to the committed keys and its ancestors."""
     tokens = np.asarray(tokens, dtype=np.int64)
     r, n, d, H = len(tokens), state.n, model.d, model.H
     if n + r > MAX_POS:
         raise ValueError("block runs past the last decoder position")
-    pos = n + np.arange(r)
+    pos = n + (np.arange(r) if parents is None else np.asarray(tree_depths(parents)))
+    self_vis = pos + 1 if parents is None else tree_visibility(parents, n)
     emb = model.w("tok_emb")[tokens] if in_rows is None else np.asarray(in_rows, np.float64)
     x = emb + model.w("pos_emb")[pos]
     tapped = {}
@@ -177,7 +205,7 @@ def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None
         v = store(qkv[:, 2 * d:], model.kv_dtype).reshape(r, H, HEAD)
         K = np.concatenate([state.self_kv[layer][0], k])
         V = np.concatenate([state.self_kv[layer][1], v])
-        a = attention(q, K, V, visible=pos + 1).reshape(r, d)
+        a = attention(q, K, V, visible=self_vis).reshape(r, d)
         x = x + a @ model.lw(layer, "w_o").T + model.lw(layer, "b_o")
 
         h = layer_norm(x, model.lw(layer, "ln2_g"), model.lw(layer, "ln2_b"))
@@ -313,3 +341,39 @@ def verify_with_anchor(model: Model, state: SeqState, drafts, layer: int):
     res = VerifyOut(greedy, a, emitted_tokens(greedy, a), margins, out.logits, out.hidden,
                     commit(state, out, a, greedy[a]), out.new_kv)
     return res, anchor_of(out.xattn[a])
+
+
+# ---------------------------------------------------------------------- tree verification
+
+@dataclass
+class TreeVerifyOut:
+    greedy: list          # g at every node
+    margins: list
+    path: list            # accepted node indices from the root: [0, u_1, .., u_a]
+    accepted: int         # a
+    emitted: list         # g along the path: a accepted drafts plus the target's token
+    state: SeqState       # committed: the path's keys / values at positions n .. n + a
+
+
+def verify_tree(model: Model, state: SeqState, tokens, parents) -> TreeVerifyOut:
+    """Verify a draft tree in one pass (appendix "Tree-decoder implementation check":
+    all nodes in one pass with a tree attention mask).  tokens[0] is the pending token
+    at the root, tokens[i] the draft of node i with parent parents[i] < i.  From the root,
+    the walk moves to the child whose token equals the current node's greedy token (the
+    lowest-index such child); the accepted drafts are the nodes passed, the emitted
+    tokens the greedy tokens along the path, and the committed cache holds the path."""
+    tokens = [int(t) for t in tokens]
+    out = forward_block(model, state, tokens, parents=parents)
+    greedy, margins = decide(out.logits)
+    path = [0]
+    while True:
+        u = path[-1]
+        nxt = [c for c in range(1, len(tokens)) if int(parents[c]) == u and tokens[c] == greedy[u]]
+        if not nxt:
+            break
+        path.append(nxt[0])
+    a = len(path) - 1
+    kv = [(np.concatenate([K, k[path]]), np.concatenate([V, v[path]]))
+          for (K, V), (k, v) in zip(state.self_kv, out.new_kv)]
+    return TreeVerifyOut(greedy, margins, path, a, [greedy[u] for u in path],
+                         SeqState(kv, state.cross, greedy[path[-1]]))
