@@ -62,6 +62,7 @@ typedef enum { AD_PADDED = 0, AD_PACKED = 1 } ad_layout;
 #define AD_ERR_TOKEN 4    /* token id outside [0, vocab)                           */
 #define AD_ERR_FRAMES 8   /* T_b outside [1, max_frames] or past frames_cap        */
 #define AD_ERR_NONFINITE 16 /* NaN/Inf logits at a valid row                       */
+#define AD_ERR_TREE 32    /* draft-tree parent not an earlier row of the block     */
 
 #define AD_HEAD_DIM 64    /* every attention head is 64 wide (score scale 1/8)     */
 #define AD_PAGE_TOKENS 16 /* tokens per self-KV page                               */
@@ -157,7 +158,7 @@ typedef struct {
 typedef struct {
   int32_t batch;              /* B >= 1                                              */
   int32_t layout;             /* ad_layout                                           */
-  int32_t k_max;              /* max draft length, 0 <= k_max < max_pos; bf16 models:
+  int32_t k_max;              /* max draft length, 0 <= k_max < max_pos and
                                  k_max <= 63 (AD_EUNSUPPORTED otherwise)               */
   int32_t rows;               /* PADDED: B*(k_max+1); PACKED: sum_b (k_b + 1)        */
   const int32_t* tokens;      /* device [rows]: per sequence t0, d_1 .. d_{k_b}      */
@@ -197,6 +198,21 @@ typedef struct {
   const int32_t* cross_window; /* device [B][2] (optional)                           */
   int32_t tap_layers[3];      /* layer indices, -1 for none                          */
   float* out_taps;            /* device [3][rows][d_model] out (optional)            */
+  /* Draft trees (optional; paper, appendix "Tree-decoder implementation check": all
+   * nodes of a candidate tree verified in one pass under a tree attention mask).  With
+   * parents given, block row i >= 1 of sequence b is a tree node whose parent is row
+   * p = parents[row0_b + i] of the same block, 0 <= p < i (AD_ERR_TREE otherwise; the
+   * entry of row 0, the root holding the pending token, is ignored).  Node i sits at
+   * position n_b + depth(i) and attends to the committed cache, its ancestors and
+   * itself; its keys / values go to cache slot n_b + i.  The accept scan walks from the
+   * root, each time to the lowest-index child whose token equals the current node's
+   * greedy token: a_b = the number of moves, out_tokens[b] = the greedy tokens along the
+   * path, out_path[b][j] = the path's j-th row (0 = root) for j <= a_b, then -1.  The
+   * anchor readout uses row out_path[b][a_b].  Commit with ad_kv_commit_tree, which also
+   * moves the path's keys / values to slots n_b .. n_b + a_b.  A chain (parents[i] =
+   * i - 1) gives exactly the results of parents = NULL.                               */
+  const int32_t* parents;     /* device [rows] (optional)                            */
+  int32_t* out_path;          /* device [B][k_max+1] out (required with parents)     */
 } ad_step;
 
 /* Bytes of workspace a step with up to max_rows rows, max_batch sequences and draft
@@ -265,6 +281,20 @@ ad_status ad_draft_input(const ad_model* target, const void* w_fuse, const void*
  * drafts; they are never read and are overwritten by the next round.
  */
 ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch, void* stream);
+
+/*
+ * Commit after a draft-tree step (paper, appendix "Tree-decoder implementation check"):
+ * for every sequence with accept_len[b] >= 0, the keys / values of accepted path node j
+ * (written at slot n_b + path[b * path_stride + j]) are moved to slot n_b + j, every
+ * layer and head, for j = 1 .. accept_len[b] (in path order: path rows increase, so no
+ * slot is overwritten before it is read), then kv_len[b] += accept_len[b] + 1.  The
+ * cache then holds what a chain step over the path's tokens would have written.  path
+ * is the step's out_path (path_stride = k_max + 1); kv is the step's cache.
+ * Errors: AD_EINVAL (NULL argument), AD_ERANGE (batch, path_stride or the cache sizes
+ * not positive).
+ */
+ad_status ad_kv_commit_tree(const ad_model* model, const ad_kv* kv, const int32_t* accept_len,
+                            const int32_t* path, int32_t path_stride, int32_t batch, void* stream);
 
 /*
  * Next draft block from linear draft heads on the final hidden state.  For sequence b

@@ -47,7 +47,7 @@ class Step(ctypes.Structure):
                 ("err_flag", _ptr), ("workspace", _ptr), ("workspace_bytes", _size),
                 ("anchor_layer", _i32), ("out_anchor", _ptr), ("out_anchor_peak", _ptr),
                 ("in_rows", _ptr), ("cross_window", _ptr), ("tap_layers", _i32 * 3),
-                ("out_taps", _ptr)]
+                ("out_taps", _ptr), ("parents", _ptr), ("out_path", _ptr)]
 
 
 def _load():
@@ -66,6 +66,7 @@ def _load():
         "ad_cross_kv_prefill": (_i32, [_ptr, _ptr, ctypes.POINTER(Cross), _ptr]),
         "ad_verify_step": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
         "ad_kv_commit": (_i32, [_ptr, _ptr, _i32, _ptr]),
+        "ad_kv_commit_tree": (_i32, [_ptr, _ptr, _ptr, _ptr, _i32, _i32, _ptr]),
         "ad_draft_heads_workspace_size": (_i32, [_ptr, _i32, _i32, ctypes.POINTER(_size)]),
         "ad_draft_heads": (_i32, [_ptr, _ptr, _i32, _ptr, _i32, _i32, _ptr, _ptr, _ptr, _i32,
                                   _ptr, _ptr, _size, _ptr]),
@@ -87,7 +88,7 @@ def _load():
 LIB = _load()
 EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model_destroy",
            "ad_model_pack_size", "ad_model_pack",
-           "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit",
+           "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit", "ad_kv_commit_tree",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_draft_input_workspace_size", "ad_draft_input",
            "ad_profile_enable", "ad_profile_read")
@@ -188,6 +189,12 @@ def verify_step(model: Model, step: Step, stream=None):
 def kv_commit(kv_len, accept_len, batch: int, stream=None):
     check(LIB.ad_kv_commit(ptr(kv_len), ptr(accept_len), batch, stream_handle(stream)),
           "ad_kv_commit")
+
+
+def kv_commit_tree(model: Model, kv: KV, accept_len, path, path_stride: int, batch: int,
+                   stream=None):
+    check(LIB.ad_kv_commit_tree(model.handle, ctypes.byref(kv), ptr(accept_len), ptr(path),
+                                path_stride, batch, stream_handle(stream)), "ad_kv_commit_tree")
 
 
 def draft_heads(model: Model, heads_w, n_heads: int, hidden, layout: int, k_max: int, cu_rows,

@@ -38,7 +38,9 @@ __global__ void __launch_bounds__(256) anchor_scores_kernel(AnchorArgs a) {
   // this thread: frame t of every block of the chunk, dims j0 .. j0 + 7 (16 contiguous
   // bytes of the key layout)
   const int t = tid >> 3, g = tid & 7, j0 = g * 8;
-  const float* qp = a.q + (size_t)(s.row0 + acc) * a.d + h * kHead + j0;
+  // the last verified row: row a_b of a chain, the accepted path's last node of a tree
+  const int row = s.row0 + (a.path ? a.path[(size_t)b * a.path_stride + acc] : acc);
+  const float* qp = a.q + (size_t)row * a.d + h * kHead + j0;
   const float4 qa = *(const float4*)qp, qb = *(const float4*)(qp + 4);
   const float q[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
   const typename S::T* kb = (const typename S::T*)a.kv + cross_base(a.layer, h, a.H, a.frames_cap);

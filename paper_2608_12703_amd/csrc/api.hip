@@ -73,6 +73,7 @@ std::vector<size_t> packed_offsets(const ad_model_desc& D) {
 struct Workspace {
   ad::SeqDesc* seqs;
   ad::RowDesc* rows;
+  ad::RowTree* tree;   // [M] depth and ancestor mask of every block row
   float* x;        // residual stream [M][d]
   float* ln;       // float32 path: LayerNorm output [M][d]
   float* q;        // queries [M][d]
@@ -106,6 +107,7 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
   w.qgroups = div_up(k_max + 1, 16);
   w.seqs = (ad::SeqDesc*)take(sizeof(ad::SeqDesc) * (size_t)B);
   w.rows = (ad::RowDesc*)take(sizeof(ad::RowDesc) * (size_t)M);
+  w.tree = (ad::RowTree*)take(sizeof(ad::RowTree) * (size_t)M);
   w.x = (float*)take(4 * M * D);
   w.q = (float*)take(4 * M * D);
   w.hidden = (float*)take(4 * M * D);
@@ -186,7 +188,18 @@ ad::AnchorArgs anchor_args(const ad_model* m, const ad_step* s, const Workspace&
   a.stats = (float2*)(w.xscore + ad::anchor_score_floats(s->batch, D.n_heads, D.max_frames));
   a.out_anchor = s->out_anchor;
   a.out_peak = s->out_anchor_peak;
+  a.path = s->parents ? s->out_path : nullptr;   // a tree's last verified row: the path's end
+  a.path_stride = s->k_max + 1;
   return a;
+}
+
+// The accept scan: prefix scan of a chain, or the walk down a draft tree.
+void accept(const ad_step* s, const Workspace& w, const int* greedy, hipStream_t st) {
+  if (s->parents)
+    ad::launch_accept_tree(s->batch, s->k_max, w.seqs, s->tokens, s->parents, greedy, s->accept_len,
+                           s->out_tokens, s->out_path, st);
+  else
+    ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
 }
 
 template <class S>
@@ -196,7 +209,7 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
                  s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
                  s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
-                 s->cross.frames_cap, s->cross_window};
+                 s->cross.frames_cap, s->cross_window, s->parents, w.tree};
   ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
   ad::launch_embed<S>(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, s->in_rows, st);
 
@@ -217,7 +230,8 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     {
       ProfScope ps(m, AD_PROF_SELF_ATTN, st);
       ad::launch_self_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->kv.pool,
-                                   s->kv.num_pages, s->kv.block_table, s->kv.pages_per_seq, st);
+                                   s->kv.num_pages, s->kv.block_table, s->kv.pages_per_seq, w.tree,
+                                   st);
     }
     e.out = w.x; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, d, w.att, lp(m, l, W_O), lp(m, l, B_O), e, st);
@@ -252,7 +266,7 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   }
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
   ad::launch_argmax(M, V, logits, V, w.rows, greedy, s->out_margin, s->err_flag, st);
-  ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+  accept(s, w, greedy, st);
   if (s->anchor_layer >= 0) ad::launch_anchor<S>(anchor_args(m, s, w), s->batch, st);
 }
 
@@ -266,7 +280,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   ad::StepArgs a{s->batch, s->layout, s->k_max, s->rows, V, D.max_pos, D.max_frames,
                  s->tokens, s->k, s->cu_rows, s->kv.kv_len, s->kv.block_table,
                  s->kv.pages_per_seq, s->kv.num_pages, s->cross.enc_len, s->cross.enc_off,
-                 s->cross.frames_cap, s->cross_window};
+                 s->cross.frames_cap, s->cross_window, s->parents, w.tree};
   ad::launch_prep(a, w.seqs, w.rows, s->err_flag, st);
   ad::launch_embed_ln(M, d, w.rows, m->p[P_TOK], m->p[P_POS], w.x, s->in_rows, lp(m, 0, LN1_G),
                       lp(m, 0, LN1_B), w.afrag, RT, st);
@@ -296,7 +310,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   at.H = H; at.d = d; at.seqs = w.seqs; at.out = w.afrag; at.out_RT = RT;
   at.num_pages = s->kv.num_pages; at.block_table = s->kv.block_table;
   at.pages_per_seq = s->kv.pages_per_seq; at.frames_cap = s->cross.frames_cap;
-  at.qgroups = w.qgroups; at.qkv_part = w.gpart; at.rows = M;
+  at.qgroups = w.qgroups; at.qkv_part = w.gpart; at.rows = M; at.tree = w.tree;
 
   for (int l = 0; l < D.n_layers; ++l) {
     at.layer = l;
@@ -353,7 +367,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   gemm(ad::EPI_ARGMAX, V, d, w.afrag, -1, 0, e, AD_PROF_LM_HEAD);
   int* greedy = s->out_greedy ? s->out_greedy : w.greedy;
   ad::launch_argmax_final(M, ad::lm_records(V), w.ampart, w.rows, greedy, s->out_margin, s->err_flag, st);
-  ad::launch_accept(s->batch, s->k_max, w.seqs, s->tokens, greedy, s->accept_len, s->out_tokens, st);
+  accept(s, w, greedy, st);
   if (s->anchor_layer >= 0) {
     ProfScope ps(m, AD_PROF_ANCHOR, st);
     ad::launch_anchor<ad::BF16>(anchor_args(m, s, w), s->batch, st);
@@ -522,8 +536,9 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->layout == AD_PACKED && !s->cu_rows) return fail(AD_EINVAL, "packed layout needs cu_rows");
   if (s->batch < 1) return fail(AD_ERANGE, "batch must be >= 1");
   if (s->k_max < 0 || s->k_max + 1 > D.max_pos) return fail(AD_ERANGE, "k_max out of range");
-  if (D.dtype == AD_BF16 && s->k_max + 1 > ad::kMaxBlockRows)
-    return fail(AD_EUNSUPPORTED, "bf16 models verify at most 64 rows per sequence (k_max <= 63)");
+  if (s->k_max + 1 > ad::kMaxBlockRows)
+    return fail(AD_EUNSUPPORTED, "at most 64 rows per sequence are verified (k_max <= 63)");
+  if (s->parents && !s->out_path) return fail(AD_EINVAL, "parents need out_path");
   const long long full = (long long)s->batch * (s->k_max + 1);
   if (s->layout == AD_PADDED && s->rows != full)
     return fail(AD_ERANGE, "padded layout needs rows == batch * (k_max + 1)");
@@ -669,6 +684,27 @@ ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch
   (void)hipGetLastError();
   ad::launch_commit(batch, kv_len, accept_len, (hipStream_t)stream);
   return check_hip("ad_kv_commit");
+}
+
+ad_status ad_kv_commit_tree(const ad_model* model, const ad_kv* kv, const int32_t* accept_len,
+                            const int32_t* path, int32_t path_stride, int32_t batch, void* stream) {
+  if (!model || !kv || !kv->pool || !kv->kv_len || !kv->block_table || !accept_len || !path)
+    return fail(AD_EINVAL, "NULL argument");
+  if (batch < 1 || path_stride < 1 || kv->num_pages < 1 || kv->pages_per_seq < 1)
+    return fail(AD_ERANGE, "batch, path_stride, num_pages and pages_per_seq must be positive");
+  const ad_model_desc& D = model->desc;
+  (void)hipGetLastError();
+  hipStream_t st = (hipStream_t)stream;
+  if (D.dtype == AD_BF16)
+    ad::launch_kv_compact<ad::BF16>(batch, D.n_layers, D.n_heads, kv->kv_len, accept_len, path,
+                                    path_stride, kv->pool, kv->num_pages, kv->block_table,
+                                    kv->pages_per_seq, st);
+  else
+    ad::launch_kv_compact<ad::F32>(batch, D.n_layers, D.n_heads, kv->kv_len, accept_len, path,
+                                   path_stride, kv->pool, kv->num_pages, kv->block_table,
+                                   kv->pages_per_seq, st);
+  ad::launch_commit(batch, kv->kv_len, accept_len, st);
+  return check_hip("ad_kv_commit_tree");
 }
 
 ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross, void* stream) {

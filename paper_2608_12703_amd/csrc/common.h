@@ -200,8 +200,16 @@ struct SeqDesc {
 struct RowDesc {
   int seq;      // owning sequence, or -1 for a padding row
   int i;        // index inside the block (0 = pending token)
-  int pos;      // decoder position n + i
+  int pos;      // decoder position: n + i, or n + depth in a draft tree
   int token;    // token id (clamped into the vocabulary)
+  int slot;     // cache slot of the row's keys / values: n + i
+};
+
+// A row of a draft-tree block: its depth below the root and its ancestor mask (bit j:
+// block row j is the row itself or one of its ancestors).
+struct RowTree {
+  unsigned long long mask;
+  int depth, pad;
 };
 
 }  // namespace ad

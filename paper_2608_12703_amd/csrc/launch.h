@@ -23,6 +23,8 @@ struct StepArgs {
   const int* enc_off;
   int frames_cap;
   const int* cross_window;   // [B][2] frames [lo, hi), or NULL: all frames
+  const int* parents;        // [rows] draft-tree parents within the block, or NULL: linear
+  RowTree* tree;             // [rows] built from parents by the prep kernel
 };
 
 // Where a GEMM's epilogue sends its output.
@@ -62,6 +64,16 @@ void launch_argmax(int M, int V, const float* logits, size_t ld, const RowDesc* 
 void launch_accept(int B, int k_max, const SeqDesc* seqs, const int* tokens, const int* greedy,
                    int* accept_len, int* out_tokens, hipStream_t st);
 void launch_commit(int B, int* kv_len, const int* accept_len, hipStream_t st);
+// Draft trees: the accept scan walks the tree (parents non-NULL) and records the path.
+void launch_accept_tree(int B, int k_max, const SeqDesc* seqs, const int* tokens, const int* parents,
+                        const int* greedy, int* accept_len, int* out_tokens, int* out_path,
+                        hipStream_t st);
+// Moves the keys / values of each accepted tree path node j (block row path[j]) to cache
+// slot n + j, for every layer (before the commit moves the length).
+template <class S>
+void launch_kv_compact(int B, int L, int H, const int* kv_len, const int* accept_len, const int* path,
+                       int path_stride, void* pool, int num_pages, const int* block_table,
+                       int pages_per_seq, hipStream_t st);
 // Logical [L][2][n][H][64] <-> paged pool copy of sequence b's positions 0..n-1.
 template <class S>
 void launch_kv_copy(bool to_linear, int L, int H, int n, int b, void* lin, void* pool, int num_pages,
@@ -129,6 +141,7 @@ struct AttnArgs {
   int pages_per_seq, frames_cap;
   int chunk, max_chunks, qgroups;   // max_chunks waves per workgroup (at most 8)
   float* q_save;   // cross-attention only, may be NULL: the finished queries, [rows][d]
+  const RowTree* tree;   // self-attention of a draft-tree block (NULL: causal block)
 };
 void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st);
 
@@ -146,6 +159,8 @@ struct AnchorArgs {
   float2* stats;           // scratch [B][H][nchunks]: (max, sum of exp(score - max))
   int* out_anchor;         // [B]
   float* out_peak;         // [B] or NULL
+  const int* path;         // draft trees: [B][path_stride] accepted nodes (NULL: linear)
+  int path_stride;
 };
 size_t anchor_score_floats(int B, int H, int max_frames);     // the scores' part
 size_t anchor_scratch_floats(int B, int H, int max_frames);   // scores + statistics
@@ -195,7 +210,7 @@ void launch_sum_partials_bias(int M, int N, int nsplit, const float* P, const vo
 template <class S>
 void launch_self_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
                            float* out, const void* pool, int num_pages, const int* block_table,
-                           int pages_per_seq, hipStream_t st);
+                           int pages_per_seq, const RowTree* tree, hipStream_t st);
 template <class S>
 void launch_cross_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
                             float* out, const void* cross, int frames_cap, hipStream_t st);

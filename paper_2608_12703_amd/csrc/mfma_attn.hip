@@ -113,13 +113,15 @@ __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, 
 }
 
 // One 32-key block of the online softmax and the two products.  MASKED: the block
-// reaches past k_end or past some query's causal limit; keys a query must not see get
-// probability 0 and value slots past k_end are zeroed (stale or poisoned cache slots
-// never reach the output).  Unmasked blocks skip all of that.  Queries past the group
-// (zero rows) are computed but never stored.
+// reaches past k_end or into the block's own rows; a query sees key `key` when
+// k_lo <= key < k_end and either key < n0 (the committed cache) or bit key - n0 of its
+// row mask tm is set (its ancestors in the block and itself: the rows before it for a
+// chain).  Keys a query must not see get probability 0 and value slots past k_end are
+// zeroed (stale or poisoned cache slots never reach the output).  Unmasked blocks skip
+// all of that.  Queries past the group (zero rows) are computed but never stored.
 template <bool MASKED>
-__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int vis,
-                                             int grp, const bf16x8 (&qh)[2],
+__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int n0,
+                                             unsigned long long tm, int grp, const bf16x8 (&qh)[2],
                                              const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
                                              float& l_run) {
   float sv[8];
@@ -134,7 +136,8 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int key = blk + grp * 8 + tt * 4 + i;
-      sv[tt * 4 + i] = (!MASKED || (key >= k_lo && key < k_end && key < vis)) ? st[i] : -INFINITY;
+      const bool see = key >= k_lo && key < k_end && (key < n0 || ((tm >> ((key - n0) & 63)) & 1));
+      sv[tt * 4 + i] = (!MASKED || see) ? st[i] : -INFINITY;
     }
   }
   const float bm = rows4_max(fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
@@ -273,6 +276,7 @@ attn_mfma_kernel(AttnArgs a) {
   float4 qp[SP], kp[SP];
   uint2 qb, kbias;
   int kpg = 0;   // page of this thread's block-row item
+  unsigned long long tmask = 0;   // self: the row mask of this lane's query
 #pragma unroll
   for (int u = 0; u < SP; ++u) qp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + qe);
   qb = *(const uint2*)(a.qkv_bias + h * kHead + qj);
@@ -280,8 +284,9 @@ attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int u = 0; u < SP; ++u) kp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + ke);
     kbias = *(const uint2*)(a.qkv_bias + kcol);
-    const int pos = s.n + (k_on ? kr : 0);
-    kpg = a.block_table[(size_t)b * a.pages_per_seq + pos / kTile];
+    const int slot = s.n + (k_on ? kr : 0);
+    kpg = a.block_table[(size_t)b * a.pages_per_seq + slot / kTile];
+    tmask = a.tree[s.row0 + q0 + min(c16, nq - 1)].mask;
   }
   // keep the key loads below after the prologue loads (issue order is completion order)
   asm volatile("" ::: "memory");
@@ -314,13 +319,13 @@ attn_mfma_kernel(AttnArgs a) {
   };
   // the block rows' keys and values: into the cache (bf16) and the LDS copy
   auto put_kv = [&](int r, int kv, int j, int pg, float4 v) {
-    const int pos = s.n + r;
+    const int slot = s.n + r;   // block row r's cache slot (its position for a chain)
     uint16_t* dst = (uint16_t*)a.kv + kv_tile_base(a.layer, kv, pg, h, a.num_pages, a.H);
     const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const uint16_t e = f32_to_bf16(vv[u]);
-      dst[tile_off(kv, pos % kTile, j + u)] = e;
+      dst[tile_off(kv, slot % kTile, j + u)] = e;
       if (kv == 0) nk[r * kHead + j + u] = e;
       else nvt[(j + u) * kMaxBlockRows + r] = e;
     }
@@ -345,8 +350,8 @@ attn_mfma_kernel(AttnArgs a) {
     if (k_on) put_kv(kr, kkv, qj, min(max(kpg, 0), a.num_pages - 1), kv4);
     for (int idx = threadIdx.x + blockDim.x; idx < nrows * 32; idx += blockDim.x) {
       const int r = idx >> 5, kv = (idx >> 4) & 1, j = (idx & 15) * 4;
-      const int pos = s.n + r;
-      const int pg = min(max(a.block_table[(size_t)b * a.pages_per_seq + pos / kTile], 0), a.num_pages - 1);
+      const int slot = s.n + r;
+      const int pg = min(max(a.block_table[(size_t)b * a.pages_per_seq + slot / kTile], 0), a.num_pages - 1);
       put_kv(r, kv, j, pg, finish_proj4(a, s.row0 + r, a.d + kv * a.d + h * kHead + j));
     }
   }
@@ -356,7 +361,8 @@ attn_mfma_kernel(AttnArgs a) {
   asm volatile("" ::: "memory");
 
   if (active) {
-    const int vis = CROSS ? s.T : s.n + q0 + c16 + 1;
+    // committed keys all visible; the block's rows through the lane's row mask
+    const int n0 = CROSS ? s.T : s.n;
     // Q^T operand: query c16, dims 16 grp + 8 hh + j, scaled by 1/8 (exact)
     bf16x8 qh[2], ql[2];
     {
@@ -380,12 +386,12 @@ attn_mfma_kernel(AttnArgs a) {
       const int clean = CROSS ? k_end : min(k_end, s.n);
       auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
         if (blk + 32 <= clean && blk >= k_lo) {
-          attend_block<false>(t, blk, k_lo, k_end, vis, grp, qh, ql, o, m_run, l_run);
+          attend_block<false>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run);
         } else if (CROSS) {
-          attend_block<true>(t, blk, k_lo, k_end, vis, grp, qh, ql, o, m_run, l_run);
+          attend_block<true>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run);
         } else {
           attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
-                             vis, grp, qh, ql, o, m_run, l_run);
+                             n0, tmask, grp, qh, ql, o, m_run, l_run);
         }
       };
       for (int blk = k_beg; blk < k_end; blk += 64) {

@@ -43,6 +43,22 @@ __global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
         const int t = a.tokens[row0 + i];
         if (t < 0 || t >= a.V) e |= 4;
       }
+      // depth and ancestor mask of every block row: a draft tree's parents must be earlier
+      // rows; without a tree the rows form a chain (row i's parent is row i - 1)
+      if (!(e & 1)) {
+        for (int i = 0; i <= kb; ++i) {
+          const int p = i == 0 ? -1 : (a.parents ? a.parents[row0 + i] : i - 1);
+          if (i > 0 && (p < 0 || p >= i)) {
+            e |= 32;
+            break;
+          }
+          RowTree r;
+          r.depth = i == 0 ? 0 : a.tree[row0 + p].depth + 1;
+          r.mask = (i == 0 ? 0ull : a.tree[row0 + p].mask) | (1ull << i);
+          r.pad = 0;
+          a.tree[row0 + i] = r;
+        }
+      }
     }
     if (e) atomicOr(err, e);
     if (e & 1) row0 = 0;
@@ -68,13 +84,14 @@ __global__ void prep_row_kernel(StepArgs a, const SeqDesc* seqs, RowDesc* rows) 
     }
     i = b >= 0 ? m - a.cu_rows[b] : 0;
   }
-  RowDesc r{-1, 0, 0, 0};
+  RowDesc r{-1, 0, 0, 0, 0};
   if (b >= 0 && b < a.B) {
     const SeqDesc s = seqs[b];
     if (s.valid && i >= 0 && i <= s.k && s.row0 + i == m) {
       r.seq = b;
       r.i = i;
-      r.pos = s.n + i;
+      r.pos = s.n + a.tree[m].depth;
+      r.slot = s.n + i;
       r.token = a.tokens[m];
     }
   }
@@ -364,6 +381,73 @@ __global__ void accept_kernel(int B, int k_max, const SeqDesc* seqs, const int* 
     out_tokens[(size_t)b * (k_max + 1) + i] = (a >= 0 && i <= a) ? greedy[s.row0 + i] : -1;
 }
 
+// Draft-tree accept: from the root, move to the lowest-index child whose token equals the
+// current node's greedy token; the emitted tokens are the greedy tokens along the path.
+__global__ void accept_tree_kernel(int B, int k_max, const SeqDesc* seqs, const int* tokens,
+                                   const int* parents, const int* greedy, int* accept_len,
+                                   int* out_tokens, int* out_path) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const SeqDesc s = seqs[b];
+  int* path = out_path + (size_t)b * (k_max + 1);
+  int a = -1;
+  if (s.valid) {
+    bool ok = true;
+    for (int i = 0; i <= s.k; ++i) ok = ok && greedy[s.row0 + i] >= 0;
+    if (ok) {
+      a = 0;
+      path[0] = 0;
+      int u = 0;
+      while (true) {
+        const int g = greedy[s.row0 + u];
+        int nxt = -1;
+        for (int c = u + 1; c <= s.k && nxt < 0; ++c)
+          if (parents[s.row0 + c] == u && tokens[s.row0 + c] == g) nxt = c;
+        if (nxt < 0) break;
+        u = nxt;
+        path[++a] = u;
+      }
+    }
+  }
+  accept_len[b] = a;
+  for (int i = 0; i <= k_max; ++i) {
+    const bool on = a >= 0 && i <= a;
+    out_tokens[(size_t)b * (k_max + 1) + i] = on ? greedy[s.row0 + path[i]] : -1;
+    if (!on) path[i] = -1;
+  }
+}
+
+// Accepted tree path node j (block row path[j], slot n + path[j]) -> slot n + j, for one
+// (layer, K|V) per block.  Nodes are moved in path order: a source slot n + path[j'] with
+// j' > j is never an earlier destination (path[j'] >= j'), and each step finishes its
+// reads before the next step's writes (barrier), so no slot is overwritten before it is
+// read.
+template <class S>
+__global__ void kv_compact_kernel(int H, const int* kv_len, const int* accept_len, const int* path,
+                                  int path_stride, typename S::T* pool, int num_pages,
+                                  const int* block_table, int pages_per_seq) {
+  const int b = blockIdx.x, layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const int a = min(accept_len[b], path_stride - 1);
+  if (a <= 0) return;
+  const int n = kv_len[b];
+  const int* p = path + (size_t)b * path_stride;
+  for (int j = 1; j <= a; ++j) {
+    const int u = p[j];
+    // (a path row never precedes its index; slots past the block table are left alone)
+    if (u > j && (n + u) / kTile < pages_per_seq) {
+      const int src = n + u, dst = n + j;
+      const int ps = min(max(block_table[(size_t)b * pages_per_seq + src / kTile], 0), num_pages - 1);
+      const int pd = min(max(block_table[(size_t)b * pages_per_seq + dst / kTile], 0), num_pages - 1);
+      for (int e = threadIdx.x; e < H * kHead; e += blockDim.x) {
+        const int h = e / kHead, c = e % kHead;
+        pool[kv_tile_base(layer, kv, pd, h, num_pages, H) + tile_off(kv, dst % kTile, c)] =
+            pool[kv_tile_base(layer, kv, ps, h, num_pages, H) + tile_off(kv, src % kTile, c)];
+      }
+    }
+    __syncthreads();
+  }
+}
+
 __global__ void commit_kernel(int B, int* kv_len, const int* accept_len) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
@@ -604,6 +688,25 @@ void launch_accept(int B, int k_max, const SeqDesc* seqs, const int* tokens, con
   hipLaunchKernelGGL(accept_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, k_max, seqs, tokens,
                      greedy, accept_len, out_tokens);
 }
+
+void launch_accept_tree(int B, int k_max, const SeqDesc* seqs, const int* tokens, const int* parents,
+                        const int* greedy, int* accept_len, int* out_tokens, int* out_path,
+                        hipStream_t st) {
+  hipLaunchKernelGGL(accept_tree_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, k_max, seqs,
+                     tokens, parents, greedy, accept_len, out_tokens, out_path);
+}
+
+template <class S>
+void launch_kv_compact(int B, int L, int H, const int* kv_len, const int* accept_len, const int* path,
+                       int path_stride, void* pool, int num_pages, const int* block_table,
+                       int pages_per_seq, hipStream_t st) {
+  hipLaunchKernelGGL(kv_compact_kernel<S>, dim3(B, 2 * L), dim3(256), 0, st, H, kv_len, accept_len,
+                     path, path_stride, (typename S::T*)pool, num_pages, block_table, pages_per_seq);
+}
+template void launch_kv_compact<F32>(int, int, int, const int*, const int*, const int*, int, void*, int,
+                                     const int*, int, hipStream_t);
+template void launch_kv_compact<BF16>(int, int, int, const int*, const int*, const int*, int, void*, int,
+                                      const int*, int, hipStream_t);
 
 void launch_commit(int B, int* kv_len, const int* accept_len, hipStream_t st) {
   hipLaunchKernelGGL(commit_kernel, dim3((B + 127) / 128), dim3(128), 0, st, B, kv_len, accept_len);

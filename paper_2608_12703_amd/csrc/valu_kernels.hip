@@ -61,10 +61,10 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
         const RowDesc rd = e.rows[m];
         if (rd.seq >= 0) {
           const int c = n - e.d, kv = c / e.d, h = (c % e.d) / kHead, j = c % kHead;
-          int pg = e.block_table[(size_t)rd.seq * e.pages_per_seq + rd.pos / kTile];
+          int pg = e.block_table[(size_t)rd.seq * e.pages_per_seq + rd.slot / kTile];
           pg = min(max(pg, 0), e.num_pages - 1);
           S::st((typename S::T*)e.cache,
-                kv_tile_base(e.layer, kv, pg, h, e.num_pages, e.H) + tile_off(kv, rd.pos % kTile, j), v);
+                kv_tile_base(e.layer, kv, pg, h, e.num_pages, e.H) + tile_off(kv, rd.slot % kTile, j), v);
         }
       }
     } else if (EPI == EPI_XKV) {
@@ -114,7 +114,8 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
                                                         const SeqDesc* seqs, const float* q,
                                                         float* out, const typename S::T* kv,
                                                         int num_pages, const int* block_table,
-                                                        int pages_per_seq, int frames_cap) {
+                                                        int pages_per_seq, int frames_cap,
+                                                        const RowTree* tree) {
   __shared__ float qs[16][65];
   __shared__ float ks[64][65];
   __shared__ float vs[64][65];
@@ -131,9 +132,10 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
       const int r = i >> 6, j = i & 63;
       qs[r][j] = r < nq ? q[(size_t)(s.row0 + qg + r) * d + h * kHead + j] : 0.f;
     }
-    // cross-attention sees frames [wlo, whi) (all frames unless a window was given)
+    // cross-attention sees frames [wlo, whi) (all frames unless a window was given);
+    // self-attention every committed key and the block rows in the query's row mask
     const int lo = CROSS ? s.wlo : 0;
-    const int vis = CROSS ? s.whi : s.n + qg + qi + 1;
+    const unsigned long long tm = (!CROSS && qi < nq) ? tree[s.row0 + qg + qi].mask : 0ull;
     const int n_keys = CROSS ? s.whi : s.n + qg + nq;
     float m_run = -INFINITY, l_run = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
     for (int c0 = lo / 64 * 64; c0 < n_keys; c0 += 64) {
@@ -166,7 +168,10 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
         float acc = 0.f;
 #pragma unroll 16
         for (int j = 0; j < 64; ++j) acc = fmaf(qs[qi][j], ks[key][j], acc);
-        sc[u] = (c0 + key >= lo && c0 + key < vis && qi < nq) ? acc * 0.125f : -INFINITY;
+        const int t = c0 + key;
+        const bool see = CROSS ? (t >= lo && t < n_keys)
+                               : (t < s.n || (t < n_keys && ((tm >> (t - s.n)) & 1)));
+        sc[u] = (see && qi < nq) ? acc * 0.125f : -INFINITY;
       }
       float cm = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
 #pragma unroll
@@ -204,18 +209,18 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
 template <class S>
 void launch_self_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
                            float* out, const void* pool, int num_pages, const int* block_table,
-                           int pages_per_seq, hipStream_t st) {
+                           int pages_per_seq, const RowTree* tree, hipStream_t st) {
   hipLaunchKernelGGL((attn_valu_kernel<S, false>), dim3(H, B), dim3(256), 0, st, H, d, layer, seqs, q, out,
-                     (const typename S::T*)pool, num_pages, block_table, pages_per_seq, 0);
+                     (const typename S::T*)pool, num_pages, block_table, pages_per_seq, 0, tree);
 }
 template <class S>
 void launch_cross_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
                             float* out, const void* cross, int frames_cap, hipStream_t st) {
   hipLaunchKernelGGL((attn_valu_kernel<S, true>), dim3(H, B), dim3(256), 0, st, H, d, layer, seqs, q, out,
-                     (const typename S::T*)cross, 0, nullptr, 0, frames_cap);
+                     (const typename S::T*)cross, 0, nullptr, 0, frames_cap, nullptr);
 }
-template void launch_self_attn_valu<F32>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, hipStream_t);
-template void launch_self_attn_valu<BF16>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, hipStream_t);
+template void launch_self_attn_valu<F32>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
+template void launch_self_attn_valu<BF16>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
 template void launch_cross_attn_valu<F32>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, hipStream_t);
 template void launch_cross_attn_valu<BF16>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, hipStream_t);
 

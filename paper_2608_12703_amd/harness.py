@@ -94,6 +94,9 @@ class Session:
         self.cross_window = None
         self.tap_layers = (-1, -1, -1)
         self.out_taps = None
+        # draft trees: per-row parents of the current block (None: chains) and the path
+        self.parents = None
+        self.out_path = torch.full((batch, k_max + 1), -1, **i32)
         self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch, k_max),
                                      dtype=torch.uint8, device=device)
         self.step_struct = None
@@ -135,8 +138,10 @@ class Session:
         self.kv_len.copy_(torch.tensor(np.asarray(n), dtype=torch.int32))
 
     # ------------------------------------------------------------------ step
-    def prepare(self, blocks, layout: int | None = None):
-        """Upload the token blocks ([t0, d_1..d_k] per sequence) and build the step struct."""
+    def prepare(self, blocks, layout: int | None = None, parents=None):
+        """Upload the token blocks ([t0, d_1..d_k] per sequence) and build the step struct.
+        parents: per sequence, the parent row of each block row (entry 0 ignored) for a
+        draft-tree step, or None for chains."""
         layout = self.layout if layout is None else layout
         ks = [len(b) - 1 for b in blocks]
         assert len(blocks) == self.B and max(ks) <= self.k_max
@@ -147,9 +152,17 @@ class Session:
                 tok[b, : len(blk)] = blk
             tok = tok.reshape(-1)
             cu = None
+            if parents is not None:
+                par = np.full((self.B, self.k_max + 1), -1, np.int64)
+                for b, p in enumerate(parents):
+                    par[b, : len(p)] = p
+                par = par.reshape(-1)
         else:
             tok = np.concatenate([np.asarray(b, np.int64) for b in blocks])
             cu = torch.tensor(np.concatenate([[0], np.cumsum([k + 1 for k in ks])]), **i32)
+            if parents is not None:
+                par = np.concatenate([np.asarray(p, np.int64) for p in parents])
+        self.parents = None if parents is None else torch.tensor(par, **i32)
         self.tokens = torch.tensor(tok, **i32)
         self.k = torch.tensor(ks, **i32)
         self.cu_rows = cu
@@ -161,7 +174,8 @@ class Session:
             self.out_hidden.data_ptr(), self.out_margin.data_ptr(), self.err_flag.data_ptr(),
             self.workspace.data_ptr(), self.workspace.numel(), int(self.anchor_layer),
             self.out_anchor.data_ptr(), self.out_anchor_peak.data_ptr(), ad.ptr(self.in_rows),
-            ad.ptr(self.cross_window), (ctypes.c_int32 * 3)(*self.tap_layers), ad.ptr(self.out_taps))
+            ad.ptr(self.cross_window), (ctypes.c_int32 * 3)(*self.tap_layers), ad.ptr(self.out_taps),
+            ad.ptr(self.parents), self.out_path.data_ptr())
         self.cur_layout = layout
         return self.step_struct
 
@@ -169,10 +183,14 @@ class Session:
         ad.verify_step(self.model, self.step_struct)
 
     def commit(self):
-        ad.kv_commit(self.kv_len, self.accept_len, self.B)
+        if self.parents is not None:
+            ad.kv_commit_tree(self.model, self.kv_struct(), self.accept_len, self.out_path,
+                              self.k_max + 1, self.B)
+        else:
+            ad.kv_commit(self.kv_len, self.accept_len, self.B)
 
-    def step(self, blocks, layout: int | None = None, commit: bool = False):
-        self.prepare(blocks, layout)
+    def step(self, blocks, layout: int | None = None, commit: bool = False, parents=None):
+        self.prepare(blocks, layout, parents)
         self.run()
         if commit:
             self.commit()
@@ -194,6 +212,8 @@ class Session:
                "err": int(self.err_flag.item())}
         if self.out_logits is not None:
             out["logits"] = self.out_logits[: self.rows].cpu().numpy()
+        if self.parents is not None:
+            out["path"] = self.out_path.cpu().numpy()
         if self.anchor_layer >= 0:
             out["anchor"] = self.out_anchor.cpu().numpy()
             out["anchor_peak"] = self.out_anchor_peak.cpu().numpy()

@@ -83,7 +83,7 @@ def _step(ad, **over):
     cross = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
     s = ad.Step(2, ad.AD_PADDED, 3, 8, 0x1000, 0x1000, None, kv, cross, 0x1000, 0x1000, None, None,
                 None, None, 0x1000, 0x1000, 1 << 40, -1, None, None, None, None,
-                (ctypes.c_int32 * 3)(-1, -1, -1), None)
+                (ctypes.c_int32 * 3)(-1, -1, -1), None, None, None)
     for k, v in over.items():
         setattr(s, k, v)
     return s
@@ -110,6 +110,8 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert run(_step(ad, anchor_layer=0)) == -1                     # readout without out_anchor
     assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(-1, -1, cfg.n_layers))) == -2
     assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(0, -1, -1))) == -1   # taps without out_taps
+    assert run(_step(ad, k_max=64, rows=130)) == -5                 # 64-bit row masks: k_max <= 63
+    assert run(_step(ad, parents=0x1000)) == -1                     # a tree without out_path
     ws = ctypes.c_size_t()
     assert ad.LIB.ad_draft_input_workspace_size(h, 2, ctypes.byref(ws)) == 0
     assert ws.value >= 7 * cfg.d_model * 2 * 4
@@ -130,6 +132,9 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1
     assert ad.LIB.ad_kv_commit(0x1000, 0x1000, 0, None) == -2
     kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
+    assert ad.LIB.ad_kv_commit_tree(h, ctypes.byref(kv), 0x1000, None, 4, 2, None) == -1
+    assert ad.LIB.ad_kv_commit_tree(h, ctypes.byref(kv), 0x1000, 0x1000, 4, 0, None) == -2
+    assert ad.LIB.ad_kv_commit_tree(h, ctypes.byref(kv), 0x1000, 0x1000, 0, 2, None) == -2
     assert ad.LIB.ad_kv_import(h, ctypes.byref(kv), 0, 0x1000, 449, 0x1000, None) == -2
     assert ad.LIB.ad_kv_export(h, ctypes.byref(kv), -1, 0x1000, 3, 0x1000, None) == -2
     cross = ad.Cross(0x1000, 17, 0x1000, 0x1000)
