@@ -49,6 +49,8 @@ def parse():
                         "this layer (-2: three quarters of the depth; -1: skip)")
     p.add_argument("--draft-steps", type=int, default=6,
                    help="also time this many audio-conditioned draft steps per round (0: skip)")
+    p.add_argument("--tree", type=int, default=1,
+                   help="also time a draft-tree step (the 11-node tree) with its commit")
     p.add_argument("--copy-calibration-mb", type=int, default=0,
                    help="after the timed steps, copy a buffer of this many MiB once (a plain "
                         "copy of known size that calibrates HBM byte counters)")
@@ -272,6 +274,57 @@ def main():
         sess.prepare(blocks)
         del runner
 
+    tree = None
+    if args.tree:
+        # Draft-tree verification of an 11-node tree per sequence (root 0 -> 1, 2, 3;
+        # 1 -> 4, 5; 2 -> 6; 4 -> 7, 8; 6 -> 9; 7 -> 10) with its commit (the accepted
+        # path's keys / values moved to consecutive slots).  The greedy continuation is
+        # planted along the deepest path 0-1-4-7-10 to the same depth as the chain
+        # workload's planted acceptance, so both emit the same tokens per step.
+        parents = [-1, 0, 0, 0, 1, 1, 2, 4, 4, 6, 7]
+        deep = [1, 4, 7, 10]
+        del sess
+        torch.cuda.empty_cache()
+        ts = Session(cfg, params, wl.batch, len(parents) - 1, wl.T, layout=layout,
+                     packed_encoder=layout == ad.AD_PACKED)
+        ts.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+        for b in range(wl.batch):
+            ts.import_prefix(b, synth.make_prefix_kv(cfg, b, int(wl.n[b])))
+        ts.set_kv_len(wl.n)
+        tblocks = []
+        for b in range(wl.batch):
+            tok = np.array([wl.t0[b]] + [wl.fill_any[b][i % len(wl.fill_any[b])] if len(wl.fill_any[b])
+                                         else 0 for i in range(len(parents) - 1)], np.int64)
+            acc_b = int(res["accept_len"][b])
+            for j, u in enumerate(deep[: min(acc_b, len(deep))]):
+                tok[u] = y[b][j]
+            tblocks.append(tok)
+        ts.prepare(tblocks, parents=[parents] * wl.batch)
+        kt0 = ts.kv_len.clone()
+
+        def tree_step():
+            ts.run()
+            ts.commit()
+            ts.kv_len.copy_(kt0)
+
+        for _ in range(args.warmup):
+            tree_step()
+        torch.cuda.synchronize()
+        rt = ts.results()
+        assert rt["err"] == 0, f"device error flag {rt['err']}"
+        ev0.record(stream)
+        for _ in range(args.steps):
+            tree_step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms_t = ev0.elapsed_time(ev1) / args.steps
+        t_tokens = int(np.sum(rt["accept_len"] + 1))
+        tree = {"nodes": len(parents), "depth": 4, "ms_per_step": round(ms_t, 4),
+                "tokens_per_step": t_tokens, "value": round(t_tokens / (ms_t / 1e3), 1),
+                "step_ratio_vs_chain": round(ms_t / ms, 4), "rows": ts.rows}
+        log(f"tree step ({len(parents)} nodes): {ms_t:.3f} ms, {t_tokens} tokens/step")
+        del ts
+
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
@@ -305,6 +358,7 @@ def main():
         "cpu_baseline": cpu,
         "anchor_readout": anchor,
         "draft_step": draft,
+        "tree_step": tree,
     }
     print(json.dumps(out), flush=True)
 

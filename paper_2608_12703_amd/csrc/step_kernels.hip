@@ -45,9 +45,11 @@ __global__ void prep_seq_kernel(StepArgs a, SeqDesc* seqs, int* err) {
       }
       // depth and ancestor mask of every block row: a draft tree's parents must be earlier
       // rows; without a tree the rows form a chain (row i's parent is row i - 1)
-      if (!(e & 1)) {
+      if (!(e & 1) && !a.parents) {
+        for (int i = 0; i <= kb; ++i) a.tree[row0 + i] = RowTree{(2ull << i) - 1, i, 0};
+      } else if (!(e & 1)) {
         for (int i = 0; i <= kb; ++i) {
-          const int p = i == 0 ? -1 : (a.parents ? a.parents[row0 + i] : i - 1);
+          const int p = i == 0 ? -1 : a.parents[row0 + i];
           if (i > 0 && (p < 0 || p >= i)) {
             e |= 32;
             break;
