@@ -213,6 +213,10 @@ typedef struct {
    * i - 1) gives exactly the results of parents = NULL.                               */
   const int32_t* parents;     /* device [rows] (optional)                            */
   int32_t* out_path;          /* device [B][k_max+1] out (required with parents)     */
+  /* The cross-attention query rows of layer anchor_layer at every row (optional, needs
+   * anchor_layer >= 0): the input of ad_anchordraft_loss when the step runs the draft
+   * block over training positions.                                                  */
+  float* out_xq;              /* device [rows][d_model] out (optional)               */
 } ad_step;
 
 /* Bytes of workspace a step with up to max_rows rows, max_batch sequences and draft
@@ -295,6 +299,44 @@ ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch
  */
 ad_status ad_kv_commit_tree(const ad_model* model, const ad_kv* kv, const int32_t* accept_len,
                             const int32_t* path, int32_t path_stride, int32_t batch, void* stream);
+
+/*
+ * The AnchorDraft training objective (paper, section "Correction and Cost", paragraph
+ * "AnchorDraft Training Objective"; appendix "Training Correction with AnchorDraft",
+ * eq. anchordraft-supp) over `batch` sequences of rows_per_seq padded rows (row t of
+ * sequence b is b * rows_per_seq + t), for a bf16 draft model whose layer `layer` (its
+ * first) attends to the audio in `cross` (the draft's own ad_cross_kv_prefill):
+ *   A_{t,hj}  = softmax over frames j < T_b of (xq_{t,h} . k_{h,j}) / 8
+ *   Abar_t(j) = (1/H) sum_h A_{t,hj}
+ *   q_t(j)    = exp(-(j - c_t)^2 / (2 sigma^2)) / sum_{l < T_b} exp(-(l - c_t)^2 / (2 sigma^2))
+ *   L_anchor  = -(1/|V|) sum_{t in V} sum_{j < T_b} q_t(j) log Abar_t(j)
+ *   L_tok     = (1/|T|) sum_{t in T} (logsumexp(z_t) - z_t[y_t])
+ *   L_feat    = (1/(|T| d)) sum_{t in T} sum_i smoothL1(feat_t,i - feat_target_t,i), beta 1
+ *   L         = L_tok + 0.5 L_feat + lambda L_anchor
+ * with V the rows whose center is >= 0 and T the rows whose target is >= 0 (the paper
+ * selects lambda = 0.1, sigma = 5).  Device inputs: xq [rows][d] the layer's
+ * cross-attention query rows (ad_step.out_xq; NULL leaves the alignment term out),
+ * center [rows] (aligned frame in 0 .. T_b - 1, -1 for none), logits [rows][vocab] and
+ * feat / feat_target [rows][d] (optional), targets [rows] (next token, -1 for none;
+ * required with logits or feat).  Device outputs: out_terms[4] = {L, L_tok, L_feat,
+ * L_anchor}; optional out_row [rows] (-sum_j q_t(j) log Abar_t(j), 0 without
+ * alignment), out_dxq [rows][d] = dL/dxq, out_dlogits [rows][vocab] = dL/dlogits and
+ * out_dfeat [rows][d] = dL/dfeat.  A centre outside [-1, T_b) or a sequence with bad
+ * frames sets AD_ERR_FRAMES, a target outside [-1, vocab) AD_ERR_TOKEN; those rows are
+ * left out.  Sums run in a fixed order (repeatable results).
+ * Errors: AD_EINVAL (NULL argument or a missing companion input), AD_ERANGE (sizes,
+ * layer, sigma <= 0, lambda < 0), AD_ENOSPACE, AD_EUNSUPPORTED (float32 model).
+ */
+ad_status ad_anchordraft_loss_workspace_size(const ad_model* draft, int32_t batch,
+                                             int32_t rows_per_seq, size_t* bytes);
+ad_status ad_anchordraft_loss(const ad_model* draft, const ad_cross* cross, int32_t layer,
+                              int32_t batch, int32_t rows_per_seq, const float* xq,
+                              const int32_t* center, float sigma, float lambda,
+                              const float* logits, const int32_t* targets, const float* feat,
+                              const float* feat_target, float* out_terms, float* out_row,
+                              float* out_dxq, float* out_dlogits, float* out_dfeat,
+                              int32_t* err_flag, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /*
  * Next draft block from linear draft heads on the final hidden state.  For sequence b

@@ -15,6 +15,14 @@ What it computes (float64 throughout, written for reading, not speed):
 * ``metrics``  -- survival s_k, conditional acceptance a_k^c and mean accepted length L
   (section 3, "Speculative Loop"; appendix "Acceptance measures").
 * ``numerics`` -- storage rounding (bf16 / fp32).
+* ``draft``    -- the audio-conditioned draft step (section 3, "Models and Protocol";
+  appendix "Draft architecture", "Window geometry").
+* ``anchor_loss`` -- the AnchorDraft training objective (section "Correction and Cost",
+  paragraph "AnchorDraft Training Objective"; appendix "Training Correction with
+  AnchorDraft").
+* Tree verification and the verification-attention anchor live in ``decoder``
+  (appendix "Tree-decoder implementation check"; section "Correction and Cost",
+  paragraph "Verification-Attention Correction").
 
 Pins: every function is checked in ``tests/test_oracle_*.py`` against something other
 than itself (library routines, closed forms, brute force, the paper's printed tables).

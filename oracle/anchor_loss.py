@@ -72,11 +72,18 @@ def anchor_loss(xqs, Ks, Ts, centers, sigma: float = SIGMA, lam: float = LAMBDA)
     """The alignment term over a batch of utterances: sequence b has query rows xqs[b]
     [r_b, H*64], first-layer cross keys Ks[b] [>= T_b, H, 64], T_b = Ts[b] valid frames
     and per-row centres centers[b] [r_b] (-1: unaligned)."""
+    As = [cross_attention_probs(xq, K, int(T)) for xq, K, T in zip(xqs, Ks, Ts)]
+    return anchor_loss_from_probs(As, Ks, centers, sigma, lam)
+
+
+def anchor_loss_from_probs(As, Ks, centers, sigma: float = SIGMA, lam: float = LAMBDA) -> AnchorLossOut:
+    """The same from the attention probabilities As[b] [r_b, H, T_b] (the gradient needs
+    the keys, not the queries)."""
     n_valid = sum(int(np.sum(np.asarray(c) >= 0)) for c in centers)
     rows, abars, grads = [], [], []
-    for xq, K, T, cen in zip(xqs, Ks, Ts, centers):
-        T = int(T)
-        A = cross_attention_probs(xq, K, T)                # [r, H, T]
+    for A, K, cen in zip(As, Ks, centers):
+        A = np.asarray(A, np.float64)
+        T = A.shape[2]
         H = A.shape[1]
         abar = A.mean(axis=1)                              # [r, T]
         ell = np.zeros(len(cen))

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libad.so")
 AD_F32, AD_BF16 = 0, 1
 AD_PADDED, AD_PACKED = 0, 1
 AD_ERR_LENGTH, AD_ERR_PAGE, AD_ERR_TOKEN, AD_ERR_FRAMES, AD_ERR_NONFINITE = 1, 2, 4, 8, 16
+AD_ERR_TREE = 32
 STATUS = {0: "AD_OK", -1: "AD_EINVAL", -2: "AD_ERANGE", -3: "AD_ENOSPACE", -4: "AD_EHIP",
           -5: "AD_EUNSUPPORTED"}
 
@@ -47,7 +48,8 @@ class Step(ctypes.Structure):
                 ("err_flag", _ptr), ("workspace", _ptr), ("workspace_bytes", _size),
                 ("anchor_layer", _i32), ("out_anchor", _ptr), ("out_anchor_peak", _ptr),
                 ("in_rows", _ptr), ("cross_window", _ptr), ("tap_layers", _i32 * 3),
-                ("out_taps", _ptr), ("parents", _ptr), ("out_path", _ptr)]
+                ("out_taps", _ptr), ("parents", _ptr), ("out_path", _ptr),
+                ("out_xq", _ptr)]
 
 
 def _load():
@@ -67,6 +69,10 @@ def _load():
         "ad_verify_step": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
         "ad_kv_commit": (_i32, [_ptr, _ptr, _i32, _ptr]),
         "ad_kv_commit_tree": (_i32, [_ptr, _ptr, _ptr, _ptr, _i32, _i32, _ptr]),
+        "ad_anchordraft_loss_workspace_size": (_i32, [_ptr, _i32, _i32, ctypes.POINTER(_size)]),
+        "ad_anchordraft_loss": (_i32, [_ptr, _ptr, _i32, _i32, _i32, _ptr, _ptr, ctypes.c_float,
+                                       ctypes.c_float, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr,
+                                       _ptr, _ptr, _ptr, _ptr, _size, _ptr]),
         "ad_draft_heads_workspace_size": (_i32, [_ptr, _i32, _i32, ctypes.POINTER(_size)]),
         "ad_draft_heads": (_i32, [_ptr, _ptr, _i32, _ptr, _i32, _i32, _ptr, _ptr, _ptr, _i32,
                                   _ptr, _ptr, _size, _ptr]),
@@ -91,6 +97,7 @@ EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model
            "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit", "ad_kv_commit_tree",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_draft_input_workspace_size", "ad_draft_input",
+           "ad_anchordraft_loss_workspace_size", "ad_anchordraft_loss",
            "ad_profile_enable", "ad_profile_read")
 PROF_CROSS_ATTN, PROF_SELF_ATTN, PROF_GEMM, PROF_LM_HEAD, PROF_XQ_CROSS, PROF_XQ, PROF_ANCHOR = 1, 2, 3, 4, 5, 6, 7
 
@@ -195,6 +202,26 @@ def kv_commit_tree(model: Model, kv: KV, accept_len, path, path_stride: int, bat
                    stream=None):
     check(LIB.ad_kv_commit_tree(model.handle, ctypes.byref(kv), ptr(accept_len), ptr(path),
                                 path_stride, batch, stream_handle(stream)), "ad_kv_commit_tree")
+
+
+def anchordraft_loss_workspace_size(model: Model, batch: int, rows_per_seq: int) -> int:
+    n = _size()
+    check(LIB.ad_anchordraft_loss_workspace_size(model.handle, batch, rows_per_seq, ctypes.byref(n)),
+          "ad_anchordraft_loss_workspace_size")
+    return n.value
+
+
+def anchordraft_loss(model: Model, cross, layer: int, batch: int, rows_per_seq: int, xq, center,
+                     sigma: float, lam: float, logits, targets, feat, feat_target, out_terms,
+                     out_row, out_dxq, out_dlogits, out_dfeat, err_flag, workspace, stream=None):
+    """The AnchorDraft objective (ad.h: ad_anchordraft_loss); cross is a Cross struct or
+    None, array arguments are device tensors or None."""
+    check(LIB.ad_anchordraft_loss(
+        model.handle, None if cross is None else ctypes.byref(cross), layer, batch, rows_per_seq,
+        ptr(xq), ptr(center), sigma, lam, ptr(logits), ptr(targets), ptr(feat), ptr(feat_target),
+        ptr(out_terms), ptr(out_row), ptr(out_dxq), ptr(out_dlogits), ptr(out_dfeat), ptr(err_flag),
+        ptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
+        stream_handle(stream)), "ad_anchordraft_loss")
 
 
 def draft_heads(model: Model, heads_w, n_heads: int, hidden, layout: int, k_max: int, cu_rows,

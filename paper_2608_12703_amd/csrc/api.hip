@@ -1,6 +1,7 @@
 // C-ABI entry points of libad.so: argument validation, workspace layout and the order
 // of kernel launches that makes one verify step.
 #include <algorithm>
+#include <cmath>
 #include <string>
 #include <vector>
 
@@ -239,8 +240,11 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     ad::launch_layernorm<S>(M, d, w.x, lp(m, l, LN2_G), lp(m, l, LN2_B), w.ln, st);
     e.out = w.q; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_STORE, M, d, d, w.ln, lp(m, l, W_XQ), lp(m, l, B_XQ), e, st);
-    if (l == s->anchor_layer)
+    if (l == s->anchor_layer) {
       (void)hipMemcpyAsync(w.q_anchor, w.q, sizeof(float) * M * d, hipMemcpyDeviceToDevice, st);
+      if (s->out_xq)
+        (void)hipMemcpyAsync(s->out_xq, w.q, sizeof(float) * M * d, hipMemcpyDeviceToDevice, st);
+    }
     {
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
       ad::launch_cross_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->cross.data,
@@ -344,6 +348,8 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
       ad::launch_attn_mfma(at, s->batch, st);
     }
     xq_cross.stop();
+    if (l == s->anchor_layer && s->out_xq)
+      (void)hipMemcpyAsync(s->out_xq, w.q_anchor, sizeof(float) * M * d, hipMemcpyDeviceToDevice, st);
     gemm(ad::EPI_PARTIAL, d, d, w.afrag, l, W_XO, none, AD_PROF_GEMM);
     ad::launch_reduce_res_ln(M, d, ad::gemm_splits(d, d), w.gpart, lp(m, l, B_XO), w.x,
                              lp(m, l, LN3_G), lp(m, l, LN3_B), w.afrag, RT, nullptr, st);
@@ -539,6 +545,7 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (s->k_max + 1 > ad::kMaxBlockRows)
     return fail(AD_EUNSUPPORTED, "at most 64 rows per sequence are verified (k_max <= 63)");
   if (s->parents && !s->out_path) return fail(AD_EINVAL, "parents need out_path");
+  if (s->out_xq && s->anchor_layer < 0) return fail(AD_EINVAL, "out_xq needs anchor_layer >= 0");
   const long long full = (long long)s->batch * (s->k_max + 1);
   if (s->layout == AD_PADDED && s->rows != full)
     return fail(AD_ERANGE, "padded layout needs rows == batch * (k_max + 1)");
@@ -684,6 +691,86 @@ ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch
   (void)hipGetLastError();
   ad::launch_commit(batch, kv_len, accept_len, (hipStream_t)stream);
   return check_hip("ad_kv_commit");
+}
+
+struct LossWs {
+  size_t stats, Z, abar, lpart, tok, feat, flag, counts, bytes;
+  int nchunk, abar_ld;
+};
+LossWs loss_ws(const ad_model_desc& D, int batch, int R) {
+  LossWs w{};
+  const size_t M = (size_t)batch * R;
+  w.nchunk = ad::loss_chunks(D.max_frames);
+  w.abar_ld = (D.max_frames + 7) / 8 * 8;
+  size_t off = 0;
+  auto take = [&](size_t n) { const size_t o = off; off += align256(n); return o; };
+  w.stats = take(8 * M * D.n_heads);
+  w.Z = take(4 * M);
+  w.abar = take(4 * M * w.abar_ld);
+  w.lpart = take(4 * M * w.nchunk);
+  w.tok = take(4 * M);
+  w.feat = take(4 * M);
+  w.flag = take(4 * M);
+  w.counts = take(8);
+  w.bytes = off;
+  return w;
+}
+
+ad_status ad_anchordraft_loss_workspace_size(const ad_model* draft, int32_t batch, int32_t rows_per_seq,
+                                             size_t* bytes) {
+  if (!draft || !bytes) return fail(AD_EINVAL, "NULL argument");
+  if (batch < 1 || rows_per_seq < 1) return fail(AD_ERANGE, "batch and rows_per_seq must be >= 1");
+  *bytes = loss_ws(draft->desc, batch, rows_per_seq).bytes;
+  return AD_OK;
+}
+
+ad_status ad_anchordraft_loss(const ad_model* draft, const ad_cross* cross, int32_t layer, int32_t batch,
+                              int32_t rows_per_seq, const float* xq, const int32_t* center, float sigma,
+                              float lambda, const float* logits, const int32_t* targets,
+                              const float* feat, const float* feat_target, float* out_terms,
+                              float* out_row, float* out_dxq, float* out_dlogits, float* out_dfeat,
+                              int32_t* err_flag, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!draft || !out_terms || !err_flag || !workspace) return fail(AD_EINVAL, "NULL argument");
+  const ad_model_desc& D = draft->desc;
+  if (D.dtype != AD_BF16) return fail(AD_EUNSUPPORTED, "the loss kernels take bf16 draft models");
+  if (batch < 1 || rows_per_seq < 1) return fail(AD_ERANGE, "batch and rows_per_seq must be >= 1");
+  if (xq) {
+    if (!cross || !cross->data || !cross->enc_len || !cross->enc_off || !center)
+      return fail(AD_EINVAL, "xq needs cross (data, enc_len, enc_off) and center");
+    if (cross->frames_cap < ad::kCrossBlock || cross->frames_cap % ad::kCrossBlock)
+      return fail(AD_ERANGE, "frames_cap must be a positive multiple of 32");
+    if (layer < 0 || layer >= D.n_layers) return fail(AD_ERANGE, "layer must be a layer index");
+    if (!(sigma > 0.f) || !std::isfinite(sigma)) return fail(AD_ERANGE, "sigma must be positive");
+    if (!(lambda >= 0.f) || !std::isfinite(lambda)) return fail(AD_ERANGE, "lambda must be >= 0");
+  } else if (out_dxq || out_row) {
+    return fail(AD_EINVAL, "out_dxq and out_row need xq");
+  }
+  if ((logits || feat) && !targets) return fail(AD_EINVAL, "logits and feat need targets");
+  if (feat && !feat_target) return fail(AD_EINVAL, "feat needs feat_target");
+  if (out_dlogits && !logits) return fail(AD_EINVAL, "out_dlogits needs logits");
+  if (out_dfeat && !feat) return fail(AD_EINVAL, "out_dfeat needs feat");
+  const LossWs w = loss_ws(D, batch, rows_per_seq);
+  if (workspace_bytes < w.bytes) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(w.bytes) + " bytes");
+  char* base = (char*)workspace;
+  ad::LossArgs a{};
+  a.B = batch; a.R = rows_per_seq; a.M = batch * rows_per_seq; a.H = D.n_heads; a.d = D.d_model;
+  a.V = D.vocab; a.layer = layer; a.max_frames = D.max_frames; a.nchunk = w.nchunk;
+  a.abar_ld = w.abar_ld;
+  if (xq) {
+    a.kv = (const uint16_t*)cross->data; a.frames_cap = cross->frames_cap;
+    a.enc_len = cross->enc_len; a.enc_off = cross->enc_off;
+  }
+  a.xq = xq; a.center = center; a.sigma = sigma; a.lam = xq ? lambda : 0.f;
+  a.logits = logits; a.targets = targets; a.feat = feat; a.feat_target = feat_target;
+  a.stats = (float2*)(base + w.stats); a.Z = (float*)(base + w.Z); a.abar = (float*)(base + w.abar);
+  a.lpart = (float*)(base + w.lpart); a.tok_row = (float*)(base + w.tok);
+  a.feat_row = (float*)(base + w.feat); a.rowflag = (int*)(base + w.flag);
+  a.counts = (int*)(base + w.counts);
+  a.out_terms = out_terms; a.out_row = out_row; a.out_dxq = out_dxq; a.out_dlogits = out_dlogits;
+  a.out_dfeat = out_dfeat; a.err = err_flag;
+  (void)hipGetLastError();
+  ad::launch_anchordraft_loss(a, (hipStream_t)stream);
+  return check_hip("ad_anchordraft_loss");
 }
 
 ad_status ad_kv_commit_tree(const ad_model* model, const ad_kv* kv, const int32_t* accept_len,

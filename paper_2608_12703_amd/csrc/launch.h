@@ -163,6 +163,39 @@ struct AnchorArgs {
   int path_stride;
 };
 size_t anchor_score_floats(int B, int H, int max_frames);     // the scores' part
+// The AnchorDraft training objective over B sequences of R padded rows (row t of
+// sequence b is b * R + t; M = B * R).
+struct LossArgs {
+  int B, R, M, H, d, V, layer, frames_cap, max_frames, nchunk, abar_ld;
+  const uint16_t* kv;          // cross K/V cache (bf16)
+  const int* enc_len;
+  const int* enc_off;
+  const float* xq;             // [M][d] the layer's cross-attention queries, or NULL
+  const int* center;           // [M] aligned frame, -1 for none
+  float sigma, lam;
+  const float* logits;         // [M][V] or NULL
+  const int* targets;          // [M] next token, -1 for none (or NULL)
+  const float* feat;           // [M][d] predicted features, or NULL
+  const float* feat_target;    // [M][d]
+  // workspace
+  float2* stats;               // [M][H] softmax (max, sum)
+  float* Z;                    // [M] Gaussian normalisers
+  float* abar;                 // [M][abar_ld] head-averaged attention
+  float* lpart;                // [M][nchunk] cross-entropy partials
+  float* tok_row;              // [M]
+  float* feat_row;             // [M]
+  int* rowflag;                // [M] bit 0 aligned, bit 1 has a next token
+  int* counts;                 // [2] |V|, |T|
+  // outputs
+  float* out_terms;            // [4] L, L_tok, L_feat, L_anchor
+  float* out_row;              // [M] or NULL
+  float* out_dxq;              // [M][d] or NULL
+  float* out_dlogits;          // [M][V] or NULL
+  float* out_dfeat;            // [M][d] or NULL
+  int* err;
+};
+int loss_chunks(int max_frames);
+void launch_anchordraft_loss(const LossArgs& a, hipStream_t st);
 size_t anchor_scratch_floats(int B, int H, int max_frames);   // scores + statistics
 template <class S>
 void launch_anchor(const AnchorArgs& a, int B, hipStream_t st);

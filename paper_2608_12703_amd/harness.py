@@ -96,6 +96,7 @@ class Session:
         self.out_taps = None
         # draft trees: per-row parents of the current block (None: chains) and the path
         self.parents = None
+        self.out_xq = None      # anchor_layer's cross-attention queries [rows][d] (optional)
         self.out_path = torch.full((batch, k_max + 1), -1, **i32)
         self.workspace = torch.empty(self.model.workspace_size(self.max_rows, batch, k_max),
                                      dtype=torch.uint8, device=device)
@@ -175,7 +176,7 @@ class Session:
             self.workspace.data_ptr(), self.workspace.numel(), int(self.anchor_layer),
             self.out_anchor.data_ptr(), self.out_anchor_peak.data_ptr(), ad.ptr(self.in_rows),
             ad.ptr(self.cross_window), (ctypes.c_int32 * 3)(*self.tap_layers), ad.ptr(self.out_taps),
-            ad.ptr(self.parents), self.out_path.data_ptr())
+            ad.ptr(self.parents), self.out_path.data_ptr(), ad.ptr(self.out_xq))
         self.cur_layout = layout
         return self.step_struct
 

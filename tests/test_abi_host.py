@@ -83,7 +83,7 @@ def _step(ad, **over):
     cross = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
     s = ad.Step(2, ad.AD_PADDED, 3, 8, 0x1000, 0x1000, None, kv, cross, 0x1000, 0x1000, None, None,
                 None, None, 0x1000, 0x1000, 1 << 40, -1, None, None, None, None,
-                (ctypes.c_int32 * 3)(-1, -1, -1), None, None, None)
+                (ctypes.c_int32 * 3)(-1, -1, -1), None, None, None, None)
     for k, v in over.items():
         setattr(s, k, v)
     return s
@@ -112,6 +112,24 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert run(_step(ad, tap_layers=(ctypes.c_int32 * 3)(0, -1, -1))) == -1   # taps without out_taps
     assert run(_step(ad, k_max=64, rows=130)) == -5                 # 64-bit row masks: k_max <= 63
     assert run(_step(ad, parents=0x1000)) == -1                     # a tree without out_path
+    assert run(_step(ad, out_xq=0x1000)) == -1                      # out_xq without anchor_layer
+    # the AnchorDraft objective: argument checks before anything is enqueued
+    lw = ctypes.c_size_t()
+    assert ad.LIB.ad_anchordraft_loss_workspace_size(h, 2, 5, ctypes.byref(lw)) == 0
+    assert ad.LIB.ad_anchordraft_loss_workspace_size(h, 0, 5, ctypes.byref(lw)) == -2
+    cr = ad.Cross(0x1000, 1504 * 2, 0x1000, 0x1000)
+    loss = lambda **o: ad.LIB.ad_anchordraft_loss(
+        h, ctypes.byref(o.get("cross", cr)), o.get("layer", 0), o.get("batch", 2), 5,
+        o.get("xq", 0x1000), o.get("center", 0x1000), o.get("sigma", 5.0), o.get("lam", 0.1),
+        o.get("logits", None), o.get("targets", None), o.get("feat", None), None, 0x1000,
+        None, o.get("dxq", None), None, None, 0x1000, 0x1000, o.get("ws", lw.value), None)
+    assert loss(center=None) == -1                                  # xq without centres
+    assert loss(logits=0x1000) == -1                                # logits without targets
+    assert loss(feat=0x1000, targets=0x1000) == -1                  # feat without feat_target
+    assert loss(xq=None, dxq=0x1000) == -1                          # a query gradient without xq
+    assert loss(batch=0) == -2 and loss(layer=cfg.n_layers) == -2
+    assert loss(sigma=0.0) == -2 and loss(lam=-1.0) == -2
+    assert loss(ws=lw.value - 1) == -3
     ws = ctypes.c_size_t()
     assert ad.LIB.ad_draft_input_workspace_size(h, 2, ctypes.byref(ws)) == 0
     assert ws.value >= 7 * cfg.d_model * 2 * 4

@@ -1,0 +1,191 @@
+"""GPU parity of the AnchorDraft objective against the oracle.
+
+Paper, section "Correction and Cost", paragraph "AnchorDraft Training Objective", and
+appendix "Training Correction with AnchorDraft" (eq. anchordraft-supp).
+* The same query rows, centres, logits and features on both sides (three utterances of
+  300, 157 and 41 frames, 37 padded rows each: three 16-row tiles with a ragged one,
+  unaligned rows and rows without a next token): the four terms, every row's alignment
+  cross-entropy and the three gradients.
+* Bad centres and targets raise their error bits and drop out of the sums.
+* End to end: the draft block's forward over a block of training positions on the GPU
+  (its first layer's query rows from ad_step.out_xq, its logits and features) against
+  the oracle's forward of the same block.
+
+Tolerances.  The keys are the draft's bf16 projection of the encoder states on both
+sides; the GPU's fp32 accumulation can put a few keys one bf16 ulp away from the
+oracle's (float64) rounding.  Queries enter the score product as hi/lo bf16 pairs
+(16 significant bits) with fp32 accumulation, so a score carries ~1e-5 of its scale;
+the loss terms follow to ~1e-5 relative, the gradient for the queries (a difference
+X - cY of two sums) to ~1e-4 of its largest entry.  Bounds: terms and row losses
+2e-5 relative (+1e-6 absolute), query gradient 5e-4 of its largest entry, logit and
+feature gradients 1e-5 relative to their scale.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import anchor_loss as al
+from oracle import decoder as od
+from oracle import draft as odr
+from paper_2608_12703_amd import ad, synth
+from paper_2608_12703_amd.configs import Config
+from paper_2608_12703_amd.harness import Session
+
+pytestmark = pytest.mark.gpu
+
+UNIT = Config(name="unit_loss", n_layers=2, d_model=128, n_heads=2, d_ffn=256, vocab=1000,
+              dtype="bf16", batch=3, k=4, k_min=0, frames=300, frames_min=40, kv_max=0,
+              geo_p=0.3, seed=13)
+SIGMA, LAM = 5.0, 0.1
+
+
+def _draft_session(cfg, params, dparams, B, R, Ts):
+    dcfg = synth.draft_config(cfg)
+    p = {n: dparams[n] for n, _ in synth.param_specs(dcfg) if n not in ("tok_emb", "pos_emb")}
+    p["tok_emb"], p["pos_emb"] = params["tok_emb"], params["pos_emb"]
+    return dcfg, Session(dcfg, p, B, R - 1, Ts, want_logits=True)
+
+
+def _run_loss(sess, B, R, xq, center, logits, targets, feat, feat_target):
+    dev = "cuda"
+    M, d, V = B * R, sess.cfg.d_model, sess.cfg.vocab
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"terms": torch.zeros(4, **f32), "row": torch.zeros(M, **f32),
+           "dxq": torch.zeros(M, d, **f32), "dlogits": torch.zeros(M, V, **f32),
+           "dfeat": torch.zeros(M, d, **f32), "err": torch.zeros(1, dtype=torch.int32, device=dev)}
+    ws = torch.empty(ad.anchordraft_loss_workspace_size(sess.model, B, R), dtype=torch.uint8, device=dev)
+    T = lambda a, dt=torch.float32: torch.tensor(np.asarray(a), dtype=dt, device=dev)
+    ad.anchordraft_loss(sess.model, sess.cross_struct(), 0, B, R, xq if torch.is_tensor(xq) else T(xq),
+                        T(center, torch.int32), SIGMA, LAM, T(logits), T(targets, torch.int32), T(feat),
+                        T(feat_target), out["terms"], out["row"], out["dxq"], out["dlogits"], out["dfeat"],
+                        out["err"], ws)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def _inputs(cfg, B, R, Ts, seed):
+    g = np.random.default_rng(seed)
+    M, d, V = B * R, cfg.d_model, cfg.vocab
+    center = np.concatenate([g.integers(0, T, R) for T in Ts])
+    center[g.random(M) < 0.2] = -1
+    targets = g.integers(0, V, M)
+    targets[g.random(M) < 0.2] = -1
+    logits = (g.standard_normal((M, V)) * 3).astype(np.float32)
+    feat = (g.standard_normal((M, d)) * 1.5).astype(np.float32)
+    feat_target = g.standard_normal((M, d)).astype(np.float32)
+    return center, targets, logits, feat, feat_target
+
+
+def _check(got, want: al.ObjectiveOut, B, R, center_ok=None):
+    print(f"  terms gpu {got['terms'].tolist()} oracle {[want.total, want.tok, want.feat, want.anchor]}")
+    np.testing.assert_allclose(got["terms"], [want.total, want.tok, want.feat, want.anchor], rtol=2e-5, atol=1e-6)
+    rows = np.concatenate(want.anchor_out.row_loss)
+    np.testing.assert_allclose(got["row"], rows, rtol=2e-5, atol=1e-6)
+    dx = np.concatenate(want.anchor_out.dxq)
+    scale = np.max(np.abs(dx))
+    err = np.max(np.abs(got["dxq"] - dx))
+    print(f"  query gradient: max {scale:.3e}, error {err:.3e} ({err / scale:.2e} of max)")
+    assert err <= 5e-4 * scale
+    for key, ref in (("dlogits", want.dlogits), ("dfeat", want.dfeat)):
+        s = np.max(np.abs(ref))
+        e = np.max(np.abs(got[key] - ref))
+        print(f"  {key}: max {s:.3e}, error {e:.3e}")
+        assert e <= 1e-5 * s
+
+
+def test_objective_matches_oracle_on_the_same_inputs():
+    cfg = UNIT
+    params, dparams = synth.make_params(cfg), synth.make_draft_params(cfg)
+    B, R, Ts = 3, 37, [300, 157, 41]
+    dcfg, sess = _draft_session(cfg, params, dparams, B, R, Ts)
+    encs = [synth.make_encoder(cfg, b, T) for b, T in enumerate(Ts)]
+    sess.prefill_encoder(encs)
+    g = np.random.default_rng(3)
+    xq = (g.standard_normal((B * R, cfg.d_model)) * 8).astype(np.float32)
+    center, targets, logits, feat, feat_target = _inputs(cfg, B, R, Ts, 4)
+    got = _run_loss(sess, B, R, xq, center, logits, targets, feat, feat_target)
+    assert got["err"][0] == 0
+    bm = odr.block_model(dcfg, params, dparams)
+    Ks = [od.cross_kv(bm, e)[0][0] for e in encs]
+    want = al.objective(logits, targets, feat, feat_target,
+                        [xq[b * R:(b + 1) * R].astype(np.float64) for b in range(B)], Ks, Ts,
+                        [center[b * R:(b + 1) * R] for b in range(B)], SIGMA, LAM)
+    assert want.anchor_out.n_valid == int(np.sum(center >= 0))
+    _check(got, want, B, R)
+    # repeatable: the same call gives the same bits
+    again = _run_loss(sess, B, R, xq, center, logits, targets, feat, feat_target)
+    for k in ("terms", "row", "dxq", "dlogits", "dfeat"):
+        np.testing.assert_array_equal(got[k].view(np.uint32), again[k].view(np.uint32))
+
+
+def test_bad_centres_and_targets_are_flagged_and_dropped():
+    cfg = UNIT
+    params, dparams = synth.make_params(cfg), synth.make_draft_params(cfg)
+    B, R, Ts = 2, 20, [90, 64]
+    dcfg, sess = _draft_session(cfg, params, dparams, B, R, Ts)
+    encs = [synth.make_encoder(cfg, b, T) for b, T in enumerate(Ts)]
+    sess.prefill_encoder(encs)
+    g = np.random.default_rng(5)
+    xq = (g.standard_normal((B * R, cfg.d_model)) * 8).astype(np.float32)
+    center, targets, logits, feat, feat_target = _inputs(cfg, B, R, Ts, 6)
+    center[3], center[R + 2] = 90, 64            # one past each sequence's last frame
+    targets[5] = cfg.vocab
+    got = _run_loss(sess, B, R, xq, center, logits, targets, feat, feat_target)
+    assert got["err"][0] == (ad.AD_ERR_FRAMES | ad.AD_ERR_TOKEN)
+    c2, t2 = center.copy(), targets.copy()
+    c2[[3, R + 2]] = -1
+    t2[5] = -1
+    bm = odr.block_model(dcfg, params, dparams)
+    Ks = [od.cross_kv(bm, e)[0][0] for e in encs]
+    want = al.objective(logits, t2, feat, feat_target,
+                        [xq[b * R:(b + 1) * R].astype(np.float64) for b in range(B)], Ks, Ts,
+                        [c2[b * R:(b + 1) * R] for b in range(B)], SIGMA, LAM)
+    _check(got, want, B, R)
+
+
+def test_end_to_end_draft_forward_and_objective():
+    cfg = UNIT
+    params, dparams = synth.make_params(cfg), synth.make_draft_params(cfg)
+    B, R, Ts = 3, 24, [250, 120, 77]
+    dcfg, sess = _draft_session(cfg, params, dparams, B, R, Ts)
+    encs = [synth.make_encoder(cfg, b, T) for b, T in enumerate(Ts)]
+    sess.prefill_encoder(encs)
+    sess.set_kv_len(np.zeros(B, np.int64))
+    g = np.random.default_rng(8)
+    tokens = [g.integers(0, cfg.vocab, R) for _ in range(B)]
+    u = (g.standard_normal((B * R, cfg.d_model)) * 0.5).astype(np.float32)
+    sess.in_rows = torch.tensor(u, device="cuda")
+    sess.anchor_layer = 0
+    sess.out_xq = torch.zeros(B * R, cfg.d_model, dtype=torch.float32, device="cuda")
+    sess.step(tokens)
+    res = sess.results()
+    assert res["err"] == 0
+    center, targets, _, _, feat_target = _inputs(cfg, B, R, Ts, 9)
+    got = _run_loss(sess, B, R, sess.out_xq, center, res["logits"], targets, res["hidden"], feat_target)
+    assert got["err"][0] == 0
+    # the oracle's own forward of the same block: probabilities, logits, features
+    bm = odr.block_model(dcfg, params, dparams)
+    As, Ks, logits, hidden = [], [], [], []
+    for b in range(B):
+        cross = od.cross_kv(bm, encs[b])
+        out = od.forward_block(bm, od.new_state(bm, cross, int(tokens[b][0])), tokens[b],
+                               in_rows=u[b * R:(b + 1) * R].astype(np.float64), probe_layer=0)
+        As.append(out.xattn)
+        Ks.append(cross[0][0])
+        logits.append(out.logits)
+        hidden.append(out.hidden)
+    logits, hidden = np.concatenate(logits), np.concatenate(hidden)
+    cen = [center[b * R:(b + 1) * R] for b in range(B)]
+    an = al.anchor_loss_from_probs(As, Ks, cen, SIGMA, LAM)
+    tok, _ = al.token_loss(logits, targets)
+    feat, _ = al.feature_loss(hidden, feat_target, targets >= 0)
+    want = [tok + 0.5 * feat + LAM * an.loss, tok, feat, an.loss]
+    print(f"  terms gpu {got['terms'].tolist()} oracle {want}")
+    # the forward's activations carry ~1e-5 relative (hi/lo operands, fp32 accumulation),
+    # which moves the terms by about as much (measured: 4e-8 relative, gradient 2.5e-5)
+    np.testing.assert_allclose(got["terms"], want, rtol=1e-4, atol=1e-6)
+    np.testing.assert_allclose(got["row"], np.concatenate(an.row_loss), rtol=1e-4, atol=1e-6)
+    dx = np.concatenate(an.dxq)
+    err = np.max(np.abs(got["dxq"] - dx)) / np.max(np.abs(dx))
+    print(f"  query gradient error {err:.2e} of max")
+    assert err <= 1e-3
