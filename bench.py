@@ -51,6 +51,9 @@ def parse():
                    help="also time this many audio-conditioned draft steps per round (0: skip)")
     p.add_argument("--tree", type=int, default=1,
                    help="also time a draft-tree step (the 11-node tree) with its commit")
+    p.add_argument("--loss", type=int, default=1,
+                   help="also time the AnchorDraft objective with its gradients at a training "
+                        "batch of the draft (12 utterances x 128 positions)")
     p.add_argument("--copy-calibration-mb", type=int, default=0,
                    help="after the timed steps, copy a buffer of this many MiB once (a plain "
                         "copy of known size that calibrates HBM byte counters)")
@@ -325,6 +328,62 @@ def main():
         log(f"tree step ({len(parents)} nodes): {ms_t:.3f} ms, {t_tokens} tokens/step")
         del ts
 
+    loss = None
+    if args.loss:
+        # The AnchorDraft objective (token cross-entropy + 0.5 smooth-L1 feature term +
+        # lambda x alignment cross-entropy) and its gradients for the logits, the features
+        # and the first draft layer's query rows, over a training batch of 12 utterances
+        # (the paper's batch size) x 128 positions of the large-v3-shape draft block.
+        # Inputs are synthetic: query rows, centres (about 10% unaligned), next tokens,
+        # logits and features; the draft's cross keys come from its own prefill.
+        LB, LR = 12, 128
+        dcfg = synth.draft_config(cfg)
+        dparams = synth.make_draft_params(cfg)
+        dp = {n: dparams[n] for n, _ in synth.param_specs(dcfg) if n not in ("tok_emb", "pos_emb")}
+        dp["tok_emb"], dp["pos_emb"] = params["tok_emb"], params["pos_emb"]
+        Ts = [int(t) for t in wl.T[:LB]]
+        ls = Session(dcfg, dp, LB, 0, Ts)
+        ls.prefill_encoder([synth.make_encoder(cfg, b, Ts[b]) for b in range(LB)])
+        g = np.random.default_rng(17)
+        LM, d, V = LB * LR, dcfg.d_model, dcfg.vocab
+        dev = "cuda"
+        f32 = dict(dtype=torch.float32, device=dev)
+        xq = torch.randn(LM, d, generator=torch.Generator(device=dev).manual_seed(1), **f32) * 8
+        cen = np.concatenate([g.integers(0, T, LR) for T in Ts])
+        cen[g.random(LM) < 0.1] = -1
+        center = torch.tensor(cen, dtype=torch.int32, device=dev)
+        targets = torch.tensor(g.integers(0, V, LM), dtype=torch.int32, device=dev)
+        logits = torch.randn(LM, V, generator=torch.Generator(device=dev).manual_seed(2), **f32) * 3
+        feat = torch.randn(LM, d, generator=torch.Generator(device=dev).manual_seed(3), **f32)
+        feat_t = torch.randn(LM, d, generator=torch.Generator(device=dev).manual_seed(4), **f32)
+        terms, row = torch.zeros(4, **f32), torch.zeros(LM, **f32)
+        dxq, dlog, dfeat = torch.empty_like(xq), torch.empty_like(logits), torch.empty_like(feat)
+        lerr = torch.zeros(1, dtype=torch.int32, device=dev)
+        lws = torch.empty(ad.anchordraft_loss_workspace_size(ls.model, LB, LR), dtype=torch.uint8,
+                          device=dev)
+
+        def loss_call():
+            ad.anchordraft_loss(ls.model, ls.cross_struct(), 0, LB, LR, xq, center, 5.0, 0.1, logits,
+                                targets, feat, feat_t, terms, row, dxq, dlog, dfeat, lerr, lws)
+
+        for _ in range(args.warmup):
+            loss_call()
+        torch.cuda.synchronize()
+        assert int(lerr.item()) == 0 and bool(torch.isfinite(terms).all())
+        ev0.record(stream)
+        for _ in range(args.steps):
+            loss_call()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        us_l = ev0.elapsed_time(ev1) / args.steps * 1e3
+        key_bytes = sum(Ts) * dcfg.n_heads * 64 * 2
+        lbytes = (2 * LM * V * 4 + key_bytes + 2 * LM * d * 4 + 3 * LM * d * 4 + LM * 12)
+        loss = {"batch": LB, "positions": LR, "frames": Ts, "us_per_call": round(us_l, 2),
+                "algorithmic_bytes": lbytes, "achieved_GBps": round(lbytes / (us_l * 1e-6) / 1e9, 1),
+                "terms": [round(float(x), 5) for x in terms.tolist()]}
+        log(f"AnchorDraft objective + gradients: {us_l:.1f} us ({lbytes / (us_l * 1e-6) / 1e9:.0f} GB/s)")
+        del ls, xq, logits, dlog
+
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
@@ -359,6 +418,7 @@ def main():
         "anchor_readout": anchor,
         "draft_step": draft,
         "tree_step": tree,
+        "anchordraft_loss": loss,
     }
     print(json.dumps(out), flush=True)
 

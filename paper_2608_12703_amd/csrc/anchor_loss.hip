@@ -9,7 +9,8 @@
 // recomputed from the layer's query rows and the cross-key cache (never stored):
 //   stats   per (head, sequence, 16-row tile): softmax max / sum over all valid frames
 //   abar    per (128-frame chunk, sequence, tile): every head's probabilities summed
-//           into Abar (kept in workspace), the row's cross-entropy partial per chunk
+//           into Abar, the row's cross-entropy partial per 32-frame block, and
+//           g_j = -q_t(j) / (H Abar_t(j)) kept in workspace for the gradient
 //   dq      per (head, sequence, tile), optional: the gradient for the query rows,
 //           d l_t / d x_{t,h} = (1/8) (X - c Y) with X = sum_j A_j g_j k_j,
 //           Y = sum_j A_j k_j, c = sum_j A_j g_j, g_j = -q_t(j) / (H Abar_t(j))
@@ -26,7 +27,6 @@ namespace ad {
 namespace {
 
 constexpr int kLossThreads = 256;
-constexpr int kLossChunk = 4 * kCrossBlock;   // frames per workgroup of the Abar kernel
 constexpr int kKtStride = 68;                 // halfwords per key row of the LDS key tile
 
 struct KTile {
@@ -114,8 +114,10 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
 
 }  // namespace
 
-// Per row: validation, the Gaussian normaliser over the sequence's valid frames, the row
-// flags (bit 0 aligned, bit 1 has a next token) and the counts |V|, |T|.  One wave per row.
+// Per row: validation, the Gaussian normaliser over the sequence's valid frames and the
+// row flags (bit 0 aligned, bit 1 has a next token).  One wave per row.  Frames further
+// than 14 sigma from the centre are left out of the normaliser: their terms are below
+// e^-98, under float32's smallest normal number.
 __global__ void __launch_bounds__(kLossThreads) aloss_prep_kernel(LossArgs a) {
   const int row = blockIdx.x * (kLossThreads / kWave) + threadIdx.x / kWave, lane = threadIdx.x % kWave;
   if (row >= a.M) return;
@@ -133,7 +135,10 @@ __global__ void __launch_bounds__(kLossThreads) aloss_prep_kernel(LossArgs a) {
   float z = 0.f;
   if (av) {
     const float inv = 1.f / (2.f * a.sigma * a.sigma);
-    for (int j = lane; j < T; j += kWave) {
+    const float reach = ceilf(14.f * a.sigma);
+    const int j0 = reach < (float)T ? max(0, c - (int)reach) : 0;
+    const int j1 = reach < (float)T ? min(T, c + (int)reach + 1) : T;
+    for (int j = j0 + lane; j < j1; j += kWave) {
       const float e = (float)(j - c);
       z += expf(-e * e * inv);
     }
@@ -142,14 +147,54 @@ __global__ void __launch_bounds__(kLossThreads) aloss_prep_kernel(LossArgs a) {
   if (lane == 0) {
     a.Z[row] = z;
     a.rowflag[row] = (av ? 1 : 0) | (tv ? 2 : 0);
-    if (av) atomicAdd(&a.counts[0], 1);
-    if (tv) atomicAdd(&a.counts[1], 1);
     if (err) atomicOr(a.err, err);
   }
 }
 
+// |V| and |T| from the row flags (one workgroup, fixed order).
+__global__ void __launch_bounds__(1024) aloss_count_kernel(LossArgs a) {
+  __shared__ float red[1024 / kWave];
+  float nv = 0.f, nt = 0.f;
+  for (int row = threadIdx.x; row < a.M; row += 1024) {
+    const int f = a.rowflag[row];
+    nv += (f & 1) ? 1.f : 0.f;
+    nt += (f & 2) ? 1.f : 0.f;
+  }
+  nv = block_sum<1024 / kWave>(nv, red);
+  nt = block_sum<1024 / kWave>(nt, red);
+  if (threadIdx.x == 0) {
+    a.counts[0] = (int)nv;
+    a.counts[1] = (int)nt;
+  }
+}
+
+// Raw loads of one (head, block) step, issued together and used later: the loads of the
+// next step go out before the current one is computed (straight-line ping-pong; loads
+// complete in order, so waiting for one step leaves the next one's in flight).
+struct QRaw {
+  float4 q[4];
+};
+__device__ __forceinline__ void load_q_raw(const LossArgs& a, int row, int h, int grp, QRaw& r) {
+  const float* p = a.xq + (size_t)row * a.d + h * kHead + grp * 16;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) r.q[u] = *(const float4*)(p + 4 * u);
+}
+__device__ __forceinline__ void q_operands(const QRaw& r, bf16x8 (&qh)[2], bf16x8 (&ql)[2]) {
+  float v[16];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    v[4 * u] = r.q[u].x * 0.125f;
+    v[4 * u + 1] = r.q[u].y * 0.125f;
+    v[4 * u + 2] = r.q[u].z * 0.125f;
+    v[4 * u + 3] = r.q[u].w * 0.125f;
+  }
+  split8(v, qh[0], ql[0]);
+  split8(v + 8, qh[1], ql[1]);
+}
+
 // Softmax statistics (max, sum of exp(score - max)) of every (row, head) over all valid
-// frames.  Four waves take interleaved 32-frame blocks; their partials merge in order.
+// frames.  Four waves take interleaved 32-frame blocks, two blocks in flight per wave;
+// their partials merge in order.
 __global__ void __launch_bounds__(kLossThreads) aloss_stats_kernel(LossArgs a) {
   __shared__ float2 part[4][kWave];
   const int h = blockIdx.x, b = blockIdx.y, tile = blockIdx.z;
@@ -162,21 +207,28 @@ __global__ void __launch_bounds__(kLossThreads) aloss_stats_kernel(LossArgs a) {
   load_q(a, row, h, grp, qh, ql);
   const int nblk = (T + kCrossBlock - 1) / kCrossBlock;
   float m = -INFINITY, l = 0.f;
-  for (int blk = w; blk < nblk; blk += 4) {
-    KTile t;
-    load_k(a, h, off, blk, c16, grp, t);
+  auto step = [&](const KTile& t, int blk) __attribute__((always_inline)) {
     float sv[8];
-    scores8(t, qh, ql, blk * kCrossBlock + grp * 8, T, sv);
+    scores8(t, qh, ql, blk * kCrossBlock + grp * 8, T, sv);   // blocks past T: all -inf
     float bm = sv[0];
 #pragma unroll
     for (int i = 1; i < 8; ++i) bm = fmaxf(bm, sv[i]);
-    if (bm == -INFINITY) continue;
     const float mn = fmaxf(m, bm);
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mn);
-    l = (m == -INFINITY ? 0.f : l * __expf(m - mn)) + s;
-    m = mn;
+    const float keep = m == -INFINITY ? 0.f : __expf(m - mn);
+    l = bm == -INFINITY ? l : l * keep + s;
+    m = bm == -INFINITY ? m : mn;
+  };
+  KTile ta, tb;
+  load_k(a, h, off, min(w, nblk - 1), c16, grp, ta);
+  load_k(a, h, off, min(w + 4, nblk - 1), c16, grp, tb);
+  for (int blk = w; blk < nblk; blk += 8) {
+    step(ta, blk);
+    load_k(a, h, off, min(blk + 8, nblk - 1), c16, grp, ta);
+    step(tb, blk + 4);
+    load_k(a, h, off, min(blk + 12, nblk - 1), c16, grp, tb);
   }
   part[w][lane] = float2{m, l};
   __syncthreads();
@@ -195,70 +247,108 @@ __global__ void __launch_bounds__(kLossThreads) aloss_stats_kernel(LossArgs a) {
   }
 }
 
-// Head-averaged attention over one 128-frame chunk (one 32-frame block per wave, every
-// head in turn), stored in workspace, and each row's cross-entropy partial over the chunk.
+// Head-averaged attention over one 128-frame chunk: four waves take interleaved heads
+// (two in flight per wave), each computing the chunk's four 32-frame blocks from one
+// load of the head's query operands; the waves' sums merge in wave order and wave w
+// finishes block w: each row's cross-entropy partial, and g = -q / (H Abar) into
+// workspace (0 where q is 0 or the row has no alignment).
+constexpr int kAbarBlocks = 4;
 __global__ void __launch_bounds__(kLossThreads) aloss_abar_kernel(LossArgs a) {
-  __shared__ float part[4][16];
+  __shared__ float part[4][kAbarBlocks][8][kWave];
   const int chunk = blockIdx.x, b = blockIdx.y, tile = blockIdx.z;
   int T, off;
-  if (!seq_frames(a, b, T, off) || chunk * kLossChunk >= T) return;
+  if (!seq_frames(a, b, T, off) || chunk * kAbarBlocks * kCrossBlock >= T) return;
   const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave, c16 = lane & 15, grp = lane >> 4;
   const int r = tile * 16 + c16;
   const int row = b * a.R + min(r, a.R - 1);
   const int nblk = (T + kCrossBlock - 1) / kCrossBlock;
-  const int blk = chunk * 4 + w;
-  const bool active = blk < nblk;
-  const int blk_ld = active ? blk : nblk - 1;   // idle waves reload a valid block
-  const int key0 = blk * kCrossBlock + grp * 8;
-  float acc[8];
+  const int blk0 = chunk * kAbarBlocks;
+  float acc[kAbarBlocks][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  for (int h = 0; h < a.H; ++h) {
+  for (int q = 0; q < kAbarBlocks; ++q)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[q][i] = 0.f;
+  struct HeadRaw {
+    QRaw q;
+    KTile k[kAbarBlocks];
+    float2 st;
+  };
+  const int H = a.H;
+  auto load = [&](int h, HeadRaw& v) __attribute__((always_inline)) {
+    const int hh = min(h, H - 1);
+    load_q_raw(a, row, hh, grp, v.q);
+#pragma unroll
+    for (int q = 0; q < kAbarBlocks; ++q) load_k(a, hh, off, min(blk0 + q, nblk - 1), c16, grp, v.k[q]);
+    v.st = a.stats[(size_t)row * H + hh];
+  };
+  auto step = [&](const HeadRaw& v, bool on) __attribute__((always_inline)) {
     bf16x8 qh[2], ql[2];
-    load_q(a, row, h, grp, qh, ql);
-    KTile t;
-    load_k(a, h, off, blk_ld, c16, grp, t);
-    const float2 st = a.stats[(size_t)row * a.H + h];
-    float sv[8];
-    scores8(t, qh, ql, key0, active ? T : 0, sv);
-    const float il = 1.f / st.y;
+    q_operands(v.q, qh, ql);
+    const float il = 1.f / v.st.y;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] += sv[i] == -INFINITY ? 0.f : __expf(sv[i] - st.x) * il;
+    for (int q = 0; q < kAbarBlocks; ++q) {
+      float sv[8];
+      scores8(v.k[q], qh, ql, (blk0 + q) * kCrossBlock + grp * 8, T, sv);   // past T: -inf
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        acc[q][i] += (on && sv[i] != -INFINITY) ? __expf(sv[i] - v.st.x) * il : 0.f;
+    }
+  };
+  HeadRaw va, vb;
+  load(w, va);
+  load(w + 4, vb);
+  for (int h = w; h < H; h += 8) {
+    step(va, true);
+    load(h + 8, va);
+    step(vb, h + 4 < H);
+    load(h + 12, vb);
   }
+#pragma unroll
+  for (int q = 0; q < kAbarBlocks; ++q)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) part[w][q][i][lane] = acc[q][i];
+  __syncthreads();
+  // wave w finishes block blk0 + w
+  const int blk = blk0 + w;
+  if (blk >= nblk) return;
+  const int key0 = blk * kCrossBlock + grp * 8;
   const int flag = a.rowflag[row];
   const int c = a.center[row];
   const float z = a.Z[row];
   const float inv = 1.f / (2.f * a.sigma * a.sigma);
+  float gv[8];
   float ell = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    acc[i] = acc[i] / (float)a.H;
+    const float ab = (((part[0][w][i][lane] + part[1][w][i][lane]) + part[2][w][i][lane]) +
+                      part[3][w][i][lane]) / (float)H;
     const int j = key0 + i;
-    if (active && j < T && (flag & 1)) {
+    gv[i] = 0.f;
+    if (j < T && (flag & 1)) {
       const float q = gauss(j, c, inv, z);
-      if (q > 0.f) ell -= q * logf(acc[i]);
+      if (q > 0.f) {
+        ell -= q * logf(ab);
+        gv[i] = -q / ((float)H * ab);
+      }
     }
   }
-  if (active && r < a.R) {
-    float* dst = a.abar + (size_t)row * a.abar_ld + key0;
+  if (r < a.R) {
+    float* dst = a.gq + (size_t)row * a.g_ld + key0;
     if (key0 + 8 <= T) {
-      *(float4*)dst = float4{acc[0], acc[1], acc[2], acc[3]};
-      *(float4*)(dst + 4) = float4{acc[4], acc[5], acc[6], acc[7]};
+      *(float4*)dst = float4{gv[0], gv[1], gv[2], gv[3]};
+      *(float4*)(dst + 4) = float4{gv[4], gv[5], gv[6], gv[7]};
     } else {
       for (int i = 0; i < 8; ++i)
-        if (key0 + i < T) dst[i] = acc[i];
+        if (key0 + i < T) dst[i] = gv[i];
     }
   }
   ell = rows4_sum(ell);
-  if (grp == 0) part[w][c16] = ell;
-  __syncthreads();
-  if (threadIdx.x < 16 && tile * 16 + (int)threadIdx.x < a.R) {
-    const float s = part[0][threadIdx.x] + part[1][threadIdx.x] + part[2][threadIdx.x] + part[3][threadIdx.x];
-    a.lpart[(size_t)(b * a.R + tile * 16 + threadIdx.x) * a.nchunk + chunk] = s;
-  }
+  if (grp == 0 && r < a.R) a.lpart[(size_t)(b * a.R + r) * a.nchunk + blk] = ell;
 }
 
 // Gradient of lambda L_anchor for the query rows (0 for rows without an alignment).
+// Four waves take interleaved 32-frame blocks, two in flight per wave (keys and the
+// row's Abar values of the block); partials merge in wave order.
 __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
   __shared__ uint16_t kt[4][kCrossBlock * kKtStride];   // per wave: one block's keys, [key][dim]
   __shared__ float xy[4][2][kHead][16];                  // per wave: X, Y partials [dim][row]
@@ -279,11 +369,7 @@ __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
   load_q(a, row, h, grp, qh, ql);
   const float2 st = a.stats[(size_t)row * a.H + h];
   const float il = 1.f / st.y;
-  const int flag = a.rowflag[row];
-  const int c = a.center[row];
-  const float z = a.Z[row];
-  const float inv = 1.f / (2.f * a.sigma * a.sigma);
-  const float* abar_row = a.abar + (size_t)row * a.abar_ld;
+  const float* g_row = a.gq + (size_t)row * a.g_ld;   // g_j of the row
   const int nblk = (T + kCrossBlock - 1) / kCrossBlock;
   f32x4 X[4], Y[4];
 #pragma unroll
@@ -292,23 +378,28 @@ __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
   uint16_t* myk = kt[w];
   // this lane's two key rows of the tile (products tt = 0, 1) and its 16 dims
   const int kA = 8 * (c16 >> 2) + (c16 & 3);
-  for (int blk = w; blk < nblk; blk += 4) {
-    KTile t;
-    load_k(a, h, off, blk, c16, grp, t);
+  struct BlkRaw {
+    KTile k;
+    float4 g0, g1;   // g of the lane's 8 keys (rows of the workspace hold whole 32-frame blocks)
+  };
+  auto load = [&](int blk, BlkRaw& v) __attribute__((always_inline)) {
+    const int bl = min(blk, nblk - 1);
+    load_k(a, h, off, bl, c16, grp, v.k);
+    const float* p = g_row + bl * kCrossBlock + grp * 8;
+    v.g0 = *(const float4*)p;
+    v.g1 = *(const float4*)(p + 4);
+  };
+  auto step = [&](const BlkRaw& v, int blk) __attribute__((always_inline)) {
     const int key0 = blk * kCrossBlock + grp * 8;
     float sv[8];
-    scores8(t, qh, ql, key0, T, sv);
+    scores8(v.k, qh, ql, key0, T, sv);
+    const float gg[8] = {v.g0.x, v.g0.y, v.g0.z, v.g0.w, v.g1.x, v.g1.y, v.g1.z, v.g1.w};
     float p0[8], p1[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int j = key0 + i;
-      const bool in = j < T;
+      const bool in = key0 + i < T;
       const float A = in ? __expf(sv[i] - st.x) * il : 0.f;
-      float g = 0.f;
-      if (in && (flag & 1)) {
-        const float q = gauss(j, c, inv, z);
-        if (q > 0.f) g = -q / ((float)a.H * abar_row[j]);
-      }
+      const float g = in ? gg[i] : 0.f;   // (workspace past T is never written)
       p0[i] = A;
       p1[i] = A * g;
       cs += A * g;
@@ -316,30 +407,39 @@ __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
     // keys [key][dim] into the wave's LDS tile, then dim-major 8-key operands
     uint2* d0 = (uint2*)(myk + kA * kKtStride + grp * 16);
     uint2* d1 = (uint2*)(myk + (kA + 4) * kKtStride + grp * 16);
-    d0[0] = make_uint2(t.k00.x, t.k00.y);
-    d0[1] = make_uint2(t.k00.z, t.k00.w);
-    d0[2] = make_uint2(t.k01.x, t.k01.y);
-    d0[3] = make_uint2(t.k01.z, t.k01.w);
-    d1[0] = make_uint2(t.k10.x, t.k10.y);
-    d1[1] = make_uint2(t.k10.z, t.k10.w);
-    d1[2] = make_uint2(t.k11.x, t.k11.y);
-    d1[3] = make_uint2(t.k11.z, t.k11.w);
+    d0[0] = make_uint2(v.k.k00.x, v.k.k00.y);
+    d0[1] = make_uint2(v.k.k00.z, v.k.k00.w);
+    d0[2] = make_uint2(v.k.k01.x, v.k.k01.y);
+    d0[3] = make_uint2(v.k.k01.z, v.k.k01.w);
+    d1[0] = make_uint2(v.k.k10.x, v.k.k10.y);
+    d1[1] = make_uint2(v.k.k10.z, v.k.k10.w);
+    d1[2] = make_uint2(v.k.k11.x, v.k.k11.y);
+    d1[3] = make_uint2(v.k.k11.z, v.k.k11.w);
     bf16x8 a0h, a0l, a1h, a1l;
     split8(p0, a0h, a0l);
     split8(p1, a1h, a1l);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       const uint16_t* src = myk + (grp * 8) * kKtStride + dt * 16 + c16;
-      uint32_t v[4];
+      uint32_t kv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        v[u] = (uint32_t)src[(2 * u) * kKtStride] | ((uint32_t)src[(2 * u + 1) * kKtStride] << 16);
-      const bf16x8 kT = as_bf16x8(make_uint4(v[0], v[1], v[2], v[3]));
+        kv[u] = (uint32_t)src[(2 * u) * kKtStride] | ((uint32_t)src[(2 * u + 1) * kKtStride] << 16);
+      const bf16x8 kT = as_bf16x8(make_uint4(kv[0], kv[1], kv[2], kv[3]));
       Y[dt] = mfma_bf16(kT, a0h, Y[dt]);
       Y[dt] = mfma_bf16(kT, a0l, Y[dt]);
       X[dt] = mfma_bf16(kT, a1h, X[dt]);
       X[dt] = mfma_bf16(kT, a1l, X[dt]);
     }
+  };
+  BlkRaw va, vb;
+  load(w, va);
+  load(w + 4, vb);
+  for (int blk = w; blk < nblk; blk += 8) {
+    step(va, blk);
+    load(blk + 8, va);
+    step(vb, blk + 4);   // past the last block: every key masked, adds nothing
+    load(blk + 12, vb);
   }
   cs = rows4_sum(cs);
   if (grp == 0) cpart[w][c16] = cs;
@@ -365,7 +465,71 @@ __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
   }
 }
 
-// Token cross-entropy of one row (and its gradient): logsumexp - z[y].
+// Token cross-entropy of one row (and its gradient): logsumexp - z[y].  The row stays in
+// registers (1024 threads x kTokPer values: vocabularies up to 64 Ki): the logits are read
+// once and the gradient written once.
+constexpr int kTokThreads = 1024, kTokPer = 64;
+template <int VEC>
+__global__ void __launch_bounds__(kTokThreads) aloss_token_reg_kernel(LossArgs a) {
+  __shared__ float red[kTokThreads / kWave];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const float* z = a.logits + (size_t)row * a.V;
+  float* dz = a.out_dlogits ? a.out_dlogits + (size_t)row * a.V : nullptr;
+  if (!(a.rowflag[row] & 2)) {
+    if (dz)
+      for (int j = tid; j < a.V; j += kTokThreads) dz[j] = 0.f;
+    if (tid == 0) a.tok_row[row] = 0.f;
+    return;
+  }
+  // element u of this thread: logit (u / VEC) * VEC * 1024 + VEC * tid + u % VEC
+  auto col = [&](int u) { return (u / VEC) * VEC * kTokThreads + VEC * tid + u % VEC; };
+  float v[kTokPer];
+#pragma unroll
+  for (int u = 0; u < kTokPer; u += VEC) {
+    const int j = col(u);
+    if (VEC == 2) {
+      const float2 p = j < a.V ? *(const float2*)(z + j) : float2{-INFINITY, -INFINITY};
+      v[u] = p.x;
+      v[u + 1] = p.y;
+    } else {
+      v[u] = j < a.V ? z[j] : -INFINITY;
+    }
+  }
+  float m = v[0];
+#pragma unroll
+  for (int u = 1; u < kTokPer; ++u) m = fmaxf(m, v[u]);
+  m = wave_max(m);
+  const int w = tid / kWave, l = tid % kWave;
+  if (l == 0) red[w] = m;
+  __syncthreads();
+  float M = red[0];
+  for (int i = 1; i < kTokThreads / kWave; ++i) M = fmaxf(M, red[i]);
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < kTokPer; ++u) {
+    v[u] = v[u] == -INFINITY ? 0.f : __expf(v[u] - M);   // v now holds exp(z - M)
+    s += v[u];
+  }
+  const float S = block_sum<kTokThreads / kWave>(s, red);
+  const int y = a.targets[row];
+  if (tid == 0) a.tok_row[row] = M + logf(S) - z[y];
+  if (dz) {
+    const float inv_s = 1.f / S, inv_n = 1.f / (float)a.counts[1];
+#pragma unroll
+    for (int u = 0; u < kTokPer; u += VEC) {
+      const int j = col(u);
+      if (j >= a.V) continue;
+      if (VEC == 2) {
+        *(float2*)(dz + j) = float2{(v[u] * inv_s - (j == y ? 1.f : 0.f)) * inv_n,
+                                    (v[u + 1] * inv_s - (j + 1 == y ? 1.f : 0.f)) * inv_n};
+      } else {
+        dz[j] = (v[u] * inv_s - (j == y ? 1.f : 0.f)) * inv_n;
+      }
+    }
+  }
+}
+
+// The same for larger vocabularies: two passes over the logits.
 __global__ void __launch_bounds__(kLossThreads) aloss_token_kernel(LossArgs a) {
   __shared__ float red[2][kLossThreads / kWave];
   const int row = blockIdx.x, tid = threadIdx.x;
@@ -438,27 +602,38 @@ __global__ void __launch_bounds__(kLossThreads) aloss_feature_kernel(LossArgs a)
   if (tid == 0) a.feat_row[row] = s;
 }
 
-// Totals in a fixed order: out_row, and {L, L_tok, L_feat, L_anchor}.
-__global__ void __launch_bounds__(kLossThreads) aloss_final_kernel(LossArgs a) {
-  __shared__ float red[kLossThreads / kWave];
+// Each row's alignment cross-entropy: the sum of its block partials (one wave per row,
+// a fixed butterfly).
+__global__ void __launch_bounds__(kLossThreads) aloss_rowsum_kernel(LossArgs a) {
+  const int row = blockIdx.x * (kLossThreads / kWave) + threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  if (row >= a.M) return;
+  float ell = 0.f;
+  if (a.rowflag[row] & 1) {
+    const int T = a.enc_len[row / a.R];
+    const int nb = (T + kCrossBlock - 1) / kCrossBlock;
+    const float* p = a.lpart + (size_t)row * a.nchunk;
+    for (int c = lane; c < nb; c += kWave) ell += p[c];
+    ell = wave_sum(ell);
+  }
+  if (lane == 0) {
+    a.lrow[row] = ell;
+    if (a.out_row) a.out_row[row] = ell;
+  }
+}
+
+// Totals in a fixed order: {L, L_tok, L_feat, L_anchor}.
+__global__ void __launch_bounds__(1024) aloss_final_kernel(LossArgs a) {
+  __shared__ float red[1024 / kWave];
   const int tid = threadIdx.x;
   float sa = 0.f, stok = 0.f, sf = 0.f;
-  for (int row = tid; row < a.M; row += kLossThreads) {
-    const int flag = a.rowflag[row];
-    float ell = 0.f;
-    if (flag & 1) {
-      const int T = a.enc_len[row / a.R];
-      const int nch = (T + kLossChunk - 1) / kLossChunk;
-      for (int c = 0; c < nch; ++c) ell += a.lpart[(size_t)row * a.nchunk + c];
-    }
-    if (a.out_row) a.out_row[row] = ell;
-    sa += ell;
+  for (int row = tid; row < a.M; row += 1024) {
+    if (a.xq) sa += a.lrow[row];
     if (a.logits) stok += a.tok_row[row];
     if (a.feat) sf += a.feat_row[row];
   }
-  sa = block_sum<kLossThreads / kWave>(sa, red);
-  stok = block_sum<kLossThreads / kWave>(stok, red);
-  sf = block_sum<kLossThreads / kWave>(sf, red);
+  sa = block_sum<1024 / kWave>(sa, red);
+  stok = block_sum<1024 / kWave>(stok, red);
+  sf = block_sum<1024 / kWave>(sf, red);
   if (tid == 0) {
     const int nv = a.counts[0], nt = a.counts[1];
     const float la = nv > 0 ? sa / (float)nv : 0.f;
@@ -471,21 +646,28 @@ __global__ void __launch_bounds__(kLossThreads) aloss_final_kernel(LossArgs a) {
   }
 }
 
-int loss_chunks(int max_frames) { return (max_frames + kLossChunk - 1) / kLossChunk; }
+int loss_chunks(int max_frames) { return (max_frames + kCrossBlock - 1) / kCrossBlock; }
 
 void launch_anchordraft_loss(const LossArgs& a, hipStream_t st) {
-  launch_zero_i32(a.counts, 2, st);
   const int tiles = (a.R + 15) / 16;
   hipLaunchKernelGGL(aloss_prep_kernel, dim3((a.M + 3) / 4), dim3(kLossThreads), 0, st, a);
+  hipLaunchKernelGGL(aloss_count_kernel, dim3(1), dim3(1024), 0, st, a);
   if (a.xq) {
     hipLaunchKernelGGL(aloss_stats_kernel, dim3(a.H, a.B, tiles), dim3(kLossThreads), 0, st, a);
-    hipLaunchKernelGGL(aloss_abar_kernel, dim3(a.nchunk, a.B, tiles), dim3(kLossThreads), 0, st, a);
+    hipLaunchKernelGGL(aloss_abar_kernel, dim3((a.nchunk + kAbarBlocks - 1) / kAbarBlocks, a.B, tiles),
+                       dim3(kLossThreads), 0, st, a);
     if (a.out_dxq)
       hipLaunchKernelGGL(aloss_dq_kernel, dim3(a.H, a.B, tiles), dim3(kLossThreads), 0, st, a);
   }
-  if (a.logits) hipLaunchKernelGGL(aloss_token_kernel, dim3(a.M), dim3(kLossThreads), 0, st, a);
+  if (a.logits && a.V <= kTokThreads * kTokPer && a.V % 2 == 0)
+    hipLaunchKernelGGL(aloss_token_reg_kernel<2>, dim3(a.M), dim3(kTokThreads), 0, st, a);
+  else if (a.logits && a.V <= kTokThreads * kTokPer)
+    hipLaunchKernelGGL(aloss_token_reg_kernel<1>, dim3(a.M), dim3(kTokThreads), 0, st, a);
+  else if (a.logits)
+    hipLaunchKernelGGL(aloss_token_kernel, dim3(a.M), dim3(kLossThreads), 0, st, a);
   if (a.feat) hipLaunchKernelGGL(aloss_feature_kernel, dim3(a.M), dim3(kLossThreads), 0, st, a);
-  hipLaunchKernelGGL(aloss_final_kernel, dim3(1), dim3(kLossThreads), 0, st, a);
+  if (a.xq) hipLaunchKernelGGL(aloss_rowsum_kernel, dim3((a.M + 3) / 4), dim3(kLossThreads), 0, st, a);
+  hipLaunchKernelGGL(aloss_final_kernel, dim3(1), dim3(1024), 0, st, a);
 }
 
 }  // namespace ad

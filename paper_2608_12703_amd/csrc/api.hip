@@ -694,20 +694,21 @@ ad_status ad_kv_commit(int32_t* kv_len, const int32_t* accept_len, int32_t batch
 }
 
 struct LossWs {
-  size_t stats, Z, abar, lpart, tok, feat, flag, counts, bytes;
-  int nchunk, abar_ld;
+  size_t stats, Z, gq, lpart, lrow, tok, feat, flag, counts, bytes;
+  int nchunk, g_ld;
 };
 LossWs loss_ws(const ad_model_desc& D, int batch, int R) {
   LossWs w{};
   const size_t M = (size_t)batch * R;
   w.nchunk = ad::loss_chunks(D.max_frames);
-  w.abar_ld = (D.max_frames + 7) / 8 * 8;
+  w.g_ld = (D.max_frames + 31) / 32 * 32;   // whole 32-frame blocks per row
   size_t off = 0;
   auto take = [&](size_t n) { const size_t o = off; off += align256(n); return o; };
   w.stats = take(8 * M * D.n_heads);
   w.Z = take(4 * M);
-  w.abar = take(4 * M * w.abar_ld);
+  w.gq = take(4 * M * w.g_ld);
   w.lpart = take(4 * M * w.nchunk);
+  w.lrow = take(4 * M);
   w.tok = take(4 * M);
   w.feat = take(4 * M);
   w.flag = take(4 * M);
@@ -755,15 +756,15 @@ ad_status ad_anchordraft_loss(const ad_model* draft, const ad_cross* cross, int3
   ad::LossArgs a{};
   a.B = batch; a.R = rows_per_seq; a.M = batch * rows_per_seq; a.H = D.n_heads; a.d = D.d_model;
   a.V = D.vocab; a.layer = layer; a.max_frames = D.max_frames; a.nchunk = w.nchunk;
-  a.abar_ld = w.abar_ld;
+  a.g_ld = w.g_ld;
   if (xq) {
     a.kv = (const uint16_t*)cross->data; a.frames_cap = cross->frames_cap;
     a.enc_len = cross->enc_len; a.enc_off = cross->enc_off;
   }
   a.xq = xq; a.center = center; a.sigma = sigma; a.lam = xq ? lambda : 0.f;
   a.logits = logits; a.targets = targets; a.feat = feat; a.feat_target = feat_target;
-  a.stats = (float2*)(base + w.stats); a.Z = (float*)(base + w.Z); a.abar = (float*)(base + w.abar);
-  a.lpart = (float*)(base + w.lpart); a.tok_row = (float*)(base + w.tok);
+  a.stats = (float2*)(base + w.stats); a.Z = (float*)(base + w.Z); a.gq = (float*)(base + w.gq);
+  a.lpart = (float*)(base + w.lpart); a.lrow = (float*)(base + w.lrow); a.tok_row = (float*)(base + w.tok);
   a.feat_row = (float*)(base + w.feat); a.rowflag = (int*)(base + w.flag);
   a.counts = (int*)(base + w.counts);
   a.out_terms = out_terms; a.out_row = out_row; a.out_dxq = out_dxq; a.out_dlogits = out_dlogits;

@@ -166,7 +166,7 @@ size_t anchor_score_floats(int B, int H, int max_frames);     // the scores' par
 // The AnchorDraft training objective over B sequences of R padded rows (row t of
 // sequence b is b * R + t; M = B * R).
 struct LossArgs {
-  int B, R, M, H, d, V, layer, frames_cap, max_frames, nchunk, abar_ld;
+  int B, R, M, H, d, V, layer, frames_cap, max_frames, nchunk, g_ld;
   const uint16_t* kv;          // cross K/V cache (bf16)
   const int* enc_len;
   const int* enc_off;
@@ -180,8 +180,9 @@ struct LossArgs {
   // workspace
   float2* stats;               // [M][H] softmax (max, sum)
   float* Z;                    // [M] Gaussian normalisers
-  float* abar;                 // [M][abar_ld] head-averaged attention
-  float* lpart;                // [M][nchunk] cross-entropy partials
+  float* gq;                   // [M][g_ld] g = -q / (H Abar) per row and frame
+  float* lpart;                // [M][nchunk] cross-entropy partials per 32-frame block
+  float* lrow;                 // [M] each row's cross-entropy
   float* tok_row;              // [M]
   float* feat_row;             // [M]
   int* rowflag;                // [M] bit 0 aligned, bit 1 has a next token
