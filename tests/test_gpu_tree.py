@@ -19,7 +19,7 @@ import pytest
 import torch
 
 from oracle import decoder as od
-from paper_2608_12703_amd import synth
+from paper_2608_12703_amd import ad, synth
 from paper_2608_12703_amd.configs import Config
 from paper_2608_12703_amd.harness import Session
 
@@ -224,3 +224,46 @@ def test_tree_decoding_is_lossless():
         assert got[b][:n_tokens] == ref[b][:n_tokens]
     assert rounds < n_tokens
     torch.cuda.synchronize()
+
+
+def test_bad_parents_skip_only_their_sequence_and_packed_trees_agree():
+    cfg = UNIT
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    rng = np.random.default_rng(4)
+    trees = [TREE, random_tree(rng, 9), [-1, 0, 1], random_tree(rng, 14), [-1, 0, 0, 1]]
+    blocks = tree_blocks(cfg, model, wl, trees, rng)
+    k_max = max(len(t) for t in trees) - 1
+    # the same trees in the padded and the packed layout: identical results
+    out = {}
+    for layout in (ad.AD_PADDED, ad.AD_PACKED):
+        s = device_session(cfg, params, wl, layout=layout, k_max=k_max)
+        s.step(blocks, parents=trees)
+        r = s.results()
+        assert r["err"] == 0
+        rows = [s.row_of(b, i) for b in range(wl.batch) for i in range(len(trees[b]))]
+        out[layout] = (r, rows, [s.export_prefix(b, int(wl.n[b]) + len(trees[b])) for b in range(wl.batch)])
+    (rp, rowp, kvp), (rk, rowk, kvk) = out[ad.AD_PADDED], out[ad.AD_PACKED]
+    for key in ("accept_len", "out_tokens", "path"):
+        np.testing.assert_array_equal(rp[key], rk[key])
+    np.testing.assert_array_equal(rp["logits"][rowp].view(np.uint32), rk["logits"][rowk].view(np.uint32))
+    for b in range(wl.batch):
+        np.testing.assert_array_equal(kvp[b].view(np.uint32), kvk[b].view(np.uint32))
+    # a parent that is not an earlier row: AD_ERR_TREE, that sequence skipped, others unchanged
+    bad = [list(t) for t in trees]
+    bad[1][3] = 3                                  # its own row
+    bad[3][5] = 9                                  # a later row
+    s = device_session(cfg, params, wl, k_max=k_max)
+    s.step(blocks, parents=bad)
+    r = s.results()
+    assert r["err"] == ad.AD_ERR_TREE
+    assert r["accept_len"][1] == -1 and r["accept_len"][3] == -1
+    assert np.all(r["out_tokens"][[1, 3]] == -1) and np.all(r["path"][[1, 3]] == -1)
+    for b in (0, 2, 4):
+        assert r["accept_len"][b] == rp["accept_len"][b]
+        np.testing.assert_array_equal(r["path"][b], rp["path"][b])
+        rows = [s.row_of(b, i) for i in range(len(trees[b]))]
+        np.testing.assert_array_equal(r["logits"][rows].view(np.uint32),
+                                      rp["logits"][[rowp[sum(len(t) for t in trees[:b]) + i]
+                                                    for i in range(len(trees[b]))]].view(np.uint32))
