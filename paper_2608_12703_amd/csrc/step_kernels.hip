@@ -420,33 +420,46 @@ __global__ void accept_tree_kernel(int B, int k_max, const SeqDesc* seqs, const 
 }
 
 // Accepted tree path node j (block row path[j], slot n + path[j]) -> slot n + j, for one
-// (layer, K|V) per block.  Nodes are moved in path order: a source slot n + path[j'] with
-// j' > j is never an earlier destination (path[j'] >= j'), and each step finishes its
-// reads before the next step's writes (barrier), so no slot is overwritten before it is
-// read.
+// (layer, K|V) per block, eight nodes at a time: each thread moves the same (head, lane)
+// element of every slot, reading all eight sources before writing any destination.  A
+// source is never an earlier node's destination (path[j] >= j), so reading a batch before
+// writing it, and batches in path order, move every slot's original contents.
 template <class S>
-__global__ void kv_compact_kernel(int H, const int* kv_len, const int* accept_len, const int* path,
-                                  int path_stride, typename S::T* pool, int num_pages,
-                                  const int* block_table, int pages_per_seq) {
+__global__ void __launch_bounds__(256) kv_compact_kernel(int H, const int* kv_len, const int* accept_len,
+                                                         const int* path, int path_stride,
+                                                         typename S::T* pool, int num_pages,
+                                                         const int* block_table, int pages_per_seq) {
+  using T = typename S::T;
   const int b = blockIdx.x, layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
   const int a = min(accept_len[b], path_stride - 1);
   if (a <= 0) return;
   const int n = kv_len[b];
   const int* p = path + (size_t)b * path_stride;
-  for (int j = 1; j <= a; ++j) {
-    const int u = p[j];
-    // (a path row never precedes its index; slots past the block table are left alone)
-    if (u > j && (n + u) / kTile < pages_per_seq) {
-      const int src = n + u, dst = n + j;
+  for (int j0 = 1; j0 <= a; j0 += 8) {
+    size_t sb[8], db[8];
+    bool mv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u;
+      const int node = j <= a ? p[j] : 0;
+      // (a path row never precedes its index; slots past the block table are left alone)
+      mv[u] = j <= a && node > j && (n + node) / kTile < pages_per_seq;
+      const int src = mv[u] ? n + node : 0, dst = mv[u] ? n + j : 0;
       const int ps = min(max(block_table[(size_t)b * pages_per_seq + src / kTile], 0), num_pages - 1);
       const int pd = min(max(block_table[(size_t)b * pages_per_seq + dst / kTile], 0), num_pages - 1);
-      for (int e = threadIdx.x; e < H * kHead; e += blockDim.x) {
-        const int h = e / kHead, c = e % kHead;
-        pool[kv_tile_base(layer, kv, pd, h, num_pages, H) + tile_off(kv, dst % kTile, c)] =
-            pool[kv_tile_base(layer, kv, ps, h, num_pages, H) + tile_off(kv, src % kTile, c)];
-      }
+      sb[u] = kv_tile_base(layer, kv, ps, 0, num_pages, H) + tile_off(kv, src % kTile, 0);
+      db[u] = kv_tile_base(layer, kv, pd, 0, num_pages, H) + tile_off(kv, dst % kTile, 0);
     }
-    __syncthreads();
+    for (int e = threadIdx.x; e < H * kHead; e += blockDim.x) {
+      const int h = e / kHead, c = e % kHead;
+      const size_t off = (size_t)h * kTileElems + (tile_off(kv, 0, c));
+      T v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = mv[u] ? pool[sb[u] + off] : T();
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (mv[u]) pool[db[u] + off] = v[u];
+    }
   }
 }
 
