@@ -466,11 +466,12 @@ __global__ void __launch_bounds__(kLossThreads) aloss_dq_kernel(LossArgs a) {
 }
 
 // Token cross-entropy of one row (and its gradient): logsumexp - z[y].  The row stays in
-// registers (1024 threads x kTokPer values: vocabularies up to 64 Ki): the logits are read
-// once and the gradient written once.
-constexpr int kTokThreads = 1024, kTokPer = 64;
-template <int VEC>
-__global__ void __launch_bounds__(kTokThreads) aloss_token_reg_kernel(LossArgs a) {
+// registers (kTokThreads threads x kTokPer values): the logits are read once and the
+// gradient written once.  Up to 52 Ki logits, 512 threads x 102 values, two workgroups
+// share a CU (one's loads overlap the other's arithmetic); up to 64 Ki, 1024 x 64.
+template <int VEC, int kTokThreads, int kTokPer>
+__global__ void __launch_bounds__(kTokThreads) __attribute__((amdgpu_waves_per_eu(kTokThreads == 512 ? 4 : 1)))
+aloss_token_reg_kernel(LossArgs a) {
   __shared__ float red[kTokThreads / kWave];
   const int row = blockIdx.x, tid = threadIdx.x;
   const float* z = a.logits + (size_t)row * a.V;
@@ -659,10 +660,12 @@ void launch_anchordraft_loss(const LossArgs& a, hipStream_t st) {
     if (a.out_dxq)
       hipLaunchKernelGGL(aloss_dq_kernel, dim3(a.H, a.B, tiles), dim3(kLossThreads), 0, st, a);
   }
-  if (a.logits && a.V <= kTokThreads * kTokPer && a.V % 2 == 0)
-    hipLaunchKernelGGL(aloss_token_reg_kernel<2>, dim3(a.M), dim3(kTokThreads), 0, st, a);
-  else if (a.logits && a.V <= kTokThreads * kTokPer)
-    hipLaunchKernelGGL(aloss_token_reg_kernel<1>, dim3(a.M), dim3(kTokThreads), 0, st, a);
+  if (a.logits && a.V <= 512 * 102 && a.V % 2 == 0)
+    hipLaunchKernelGGL((aloss_token_reg_kernel<2, 512, 102>), dim3(a.M), dim3(512), 0, st, a);
+  else if (a.logits && a.V <= 1024 * 64 && a.V % 2 == 0)
+    hipLaunchKernelGGL((aloss_token_reg_kernel<2, 1024, 64>), dim3(a.M), dim3(1024), 0, st, a);
+  else if (a.logits && a.V <= 1024 * 64)
+    hipLaunchKernelGGL((aloss_token_reg_kernel<1, 1024, 64>), dim3(a.M), dim3(1024), 0, st, a);
   else if (a.logits)
     hipLaunchKernelGGL(aloss_token_kernel, dim3(a.M), dim3(kLossThreads), 0, st, a);
   if (a.feat) hipLaunchKernelGGL(aloss_feature_kernel, dim3(a.M), dim3(kLossThreads), 0, st, a);
