@@ -16,6 +16,8 @@
 //           ties).
 // Keys are read once (the layer's K of every sequence, as the attention kernel does for
 // one of its products); the scores round-trip through a small scratch buffer.
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
@@ -121,10 +123,16 @@ __global__ void __launch_bounds__(kPickThreads) anchor_pick_kernel(AnchorArgs a)
     }
     return;
   }
-  const int T = s.T, H = a.H, nch = (T + kAnchorChunk - 1) / kAnchorChunk;
+  const int T = s.T, H = a.H;
+  // fused: the scores of every block row, one (max, sum) per head; else this sequence's
+  // recomputed row, statistics per chunk
+  const size_t base = a.fused ? (size_t)s.row0 + (a.path ? a.path[(size_t)b * a.path_stride + acc] : acc)
+                              : (size_t)b;
+  const int nch = a.fused ? 1 : (T + kAnchorChunk - 1) / kAnchorChunk;
+  const int ld = a.fused ? a.score_ld : a.max_frames;
   // each head's softmax normaliser from its chunks, in chunk order
   for (int h = tid; h < H; h += kPickThreads) {
-    const float2* st = a.stats + ((size_t)b * H + h) * a.nchunks;
+    const float2* st = a.stats + (base * H + h) * (a.fused ? 1 : a.nchunks);
     float M = -INFINITY;
     for (int c = 0; c < nch; ++c) M = fmaxf(M, st[c].x);
     float L = 0.f;
@@ -136,7 +144,7 @@ __global__ void __launch_bounds__(kPickThreads) anchor_pick_kernel(AnchorArgs a)
   // head-averaged weight per frame (heads summed in order), two frames per pass and
   // eight heads' scores per round of loads; this thread's best (its frames rise, so
   // '>' keeps the lowest index among equal values)
-  const float* sc = a.score + (size_t)b * H * a.max_frames;
+  const float* sc = a.score + base * H * ld;
   float best = -1.f;
   int best_t = 0x7fffffff;
   for (int t0 = tid; t0 < T; t0 += 2 * kPickThreads) {
@@ -148,7 +156,7 @@ __global__ void __launch_bounds__(kPickThreads) anchor_pick_kernel(AnchorArgs a)
 #pragma unroll
         for (int e = 0; e < kHB; ++e) {
           const int h = min(hb + e, H - 1), t = min(t0 + f * kPickThreads, T - 1);
-          v[f][e] = sc[(size_t)h * a.max_frames + t];
+          v[f][e] = sc[(size_t)h * ld + t];
         }
 #pragma unroll
       for (int f = 0; f < 2; ++f)
@@ -193,17 +201,83 @@ __global__ void __launch_bounds__(kPickThreads) anchor_pick_kernel(AnchorArgs a)
   }
 }
 
-size_t anchor_score_floats(int B, int H, int max_frames) {
-  return ((size_t)B * H * max_frames + 63) / 64 * 64;   // the statistics follow, aligned
+// Fused readout: the head-averaged weights of one block row, a slice of frames per
+// workgroup (every frame's heads loaded at once), each slice's best (weight, lowest frame)
+// merged with a 64-bit atomic max over (weight bits, ~frame): weights are >= 0, so their
+// bits order like the values, and the result does not depend on the merge order.
+constexpr int kPickSlices = 8, kSliceThreads = 256;
+__global__ void __launch_bounds__(kSliceThreads) anchor_pick_slices_kernel(AnchorArgs a) {
+  __shared__ float Mh[64], Lh[64];
+  __shared__ unsigned long long red[kSliceThreads / kWave];
+  const int b = blockIdx.x, slice = blockIdx.y, tid = threadIdx.x;
+  const SeqDesc s = a.seqs[b];
+  const int acc = a.accept_len[b];
+  if (!s.valid || acc < 0) return;
+  const int T = s.T, H = a.H, ld = a.score_ld;
+  const size_t row = (size_t)s.row0 + (a.path ? a.path[(size_t)b * a.path_stride + acc] : acc);
+  for (int h = tid; h < H; h += kSliceThreads) {
+    const float2 st = a.stats[row * H + h];
+    Mh[h] = st.x;
+    Lh[h] = st.y;
+  }
+  __syncthreads();
+  const int per = (T + kPickSlices - 1) / kPickSlices;
+  const int t0 = slice * per, t1 = min(T, t0 + per);
+  const float* sc = a.score + row * H * ld;
+  unsigned long long best = 0;
+  for (int t = t0 + tid; t < t1; t += kSliceThreads) {
+    float w = 0.f;
+    for (int h = 0; h < H; ++h) w += expf(sc[(size_t)h * ld + t] - Mh[h]) / Lh[h];
+    w = w / (float)H;
+    const unsigned long long key =
+        ((unsigned long long)__float_as_uint(w) << 32) | (unsigned long long)(0xffffffffu - (unsigned)t);
+    best = key > best ? key : best;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const unsigned long long other = __shfl_xor(best, o, kWave);
+    best = other > best ? other : best;
+  }
+  if ((tid & 63) == 0) red[tid >> 6] = best;
+  __syncthreads();
+  if (tid == 0) {
+    for (int i = 1; i < kSliceThreads / kWave; ++i) best = red[i] > best ? red[i] : best;
+    if (best) atomicMax(a.best + b, best);
+  }
 }
 
-size_t anchor_scratch_floats(int B, int H, int max_frames) {
+// The merged best per sequence into the outputs; the slot is left at 0 for the next step.
+__global__ void anchor_pick_final_kernel(AnchorArgs a, int B) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const SeqDesc s = a.seqs[b];
+  const bool ok = s.valid && a.accept_len[b] >= 0;
+  const unsigned long long v = a.best[b];
+  a.out_anchor[b] = ok ? (int)(0xffffffffu - (unsigned)(v & 0xffffffffu)) : -1;
+  if (a.out_peak) a.out_peak[b] = ok ? __uint_as_float((unsigned)(v >> 32)) : 0.f;
+  a.best[b] = 0;
+}
+
+int anchor_score_ld(int max_frames) { return (max_frames + kCrossBlock - 1) / kCrossBlock * kCrossBlock; }
+
+size_t anchor_score_floats(int rows, int B, int H, int max_frames) {
+  const size_t n = std::max((size_t)B * H * max_frames, (size_t)rows * H * anchor_score_ld(max_frames));
+  return (n + 63) / 64 * 64;   // the statistics follow, aligned
+}
+
+size_t anchor_scratch_floats(int rows, int B, int H, int max_frames) {
   const int nch = (max_frames + kAnchorChunk - 1) / kAnchorChunk;
-  return anchor_score_floats(B, H, max_frames) + 2 * (size_t)B * H * nch;
+  return anchor_score_floats(rows, B, H, max_frames) +
+         2 * std::max((size_t)B * H * nch, (size_t)rows * H);
 }
 
 template <class S>
 void launch_anchor(const AnchorArgs& a, int B, hipStream_t st) {
+  if (a.fused) {
+    hipLaunchKernelGGL(anchor_pick_slices_kernel, dim3(B, kPickSlices), dim3(kSliceThreads), 0, st, a);
+    hipLaunchKernelGGL(anchor_pick_final_kernel, dim3((B + 255) / 256), dim3(256), 0, st, a, B);
+    return;
+  }
   hipLaunchKernelGGL(anchor_scores_kernel<S>, dim3(a.H, B, a.nchunks), dim3(256), 0, st, a);
   hipLaunchKernelGGL(anchor_pick_kernel, dim3(B), dim3(kPickThreads), 0, st, a);
 }

@@ -89,6 +89,7 @@ struct Workspace {
   void* ampart;    // bf16 path: LM-head top-2 records
   float* q_anchor; // the anchor layer's cross-attention queries [M][d]
   float* xscore;   // anchor readout scratch (scores, then per-chunk statistics)
+  unsigned long long* abest;   // fused readout: per-sequence merged best
   int RT, qgroups;
   size_t bytes;
 };
@@ -114,7 +115,8 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
   w.hidden = (float*)take(4 * M * D);
   w.greedy = (int*)take(4ull * M);
   w.q_anchor = (float*)take(4 * M * D);
-  w.xscore = (float*)take(4 * ad::anchor_scratch_floats(B, d.n_heads, d.max_frames));
+  w.xscore = (float*)take(4 * ad::anchor_scratch_floats(M, B, d.n_heads, d.max_frames));
+  w.abest = (unsigned long long*)take(8ull * B);
   if (d.dtype == AD_F32) {
     w.ln = (float*)take(4 * M * D);
     w.att = (float*)take(4 * M * D);
@@ -172,6 +174,12 @@ void copy_taps(const ad_step* s, int l, const float* x, int M, int d, hipStream_
                            hipMemcpyDeviceToDevice, st);
 }
 
+// The bf16 path keeps the anchor layer's scores in its cross-attention (no window: the
+// readout covers every frame); otherwise the readout recomputes them.
+bool anchor_fused(const ad_model* m, const ad_step* s) {
+  return m->desc.dtype == AD_BF16 && s->anchor_layer >= 0 && !s->cross_window;
+}
+
 ad::AnchorArgs anchor_args(const ad_model* m, const ad_step* s, const Workspace& w) {
   const ad_model_desc& D = m->desc;
   ad::AnchorArgs a{};
@@ -186,7 +194,10 @@ ad::AnchorArgs anchor_args(const ad_model* m, const ad_step* s, const Workspace&
   a.max_frames = D.max_frames;
   a.nchunks = div_up(D.max_frames, ad::kAnchorChunk);
   a.score = w.xscore;
-  a.stats = (float2*)(w.xscore + ad::anchor_score_floats(s->batch, D.n_heads, D.max_frames));
+  a.stats = (float2*)(w.xscore + ad::anchor_score_floats(s->rows, s->batch, D.n_heads, D.max_frames));
+  a.fused = anchor_fused(m, s);
+  a.best = w.abest;
+  a.score_ld = ad::anchor_score_ld(D.max_frames);
   a.out_anchor = s->out_anchor;
   a.out_peak = s->out_anchor_peak;
   a.path = s->parents ? s->out_path : nullptr;   // a tree's last verified row: the path's end
@@ -342,7 +353,12 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     at.max_chunks = div_up(D.max_frames, ad::kCrossChunk);
     at.qkv_splits = ad::gemm_splits(d, d); at.qkv_n = d;
     at.qkv_bias = (const uint16_t*)lp(m, l, B_XQ);
-    at.q_save = l == s->anchor_layer ? w.q_anchor : nullptr;
+    const bool fuse = l == s->anchor_layer && anchor_fused(m, s);
+    at.q_save = l == s->anchor_layer && (!fuse || s->out_xq) ? w.q_anchor : nullptr;
+    at.score_out = fuse ? w.xscore : nullptr;
+    at.stat_out = fuse ? (float2*)(w.xscore + ad::anchor_score_floats(M, s->batch, H, D.max_frames)) : nullptr;
+    at.score_ld = ad::anchor_score_ld(D.max_frames);
+    at.best_clear = fuse ? w.abest : nullptr;
     {
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
       ad::launch_attn_mfma(at, s->batch, st);

@@ -142,6 +142,12 @@ struct AttnArgs {
   int chunk, max_chunks, qgroups;   // max_chunks waves per workgroup (at most 8)
   float* q_save;   // cross-attention only, may be NULL: the finished queries, [rows][d]
   const RowTree* tree;   // self-attention of a draft-tree block (NULL: causal block)
+  // cross-attention at the anchor layer, may be NULL: every query row's scores
+  // [rows][H][score_ld] (keys past the sequence: -inf) and softmax (max, sum) [rows][H]
+  float* score_out;
+  float2* stat_out;
+  int score_ld;
+  unsigned long long* best_clear;   // [B] zeroed here for the readout's merge (or NULL)
 };
 void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st);
 
@@ -161,8 +167,15 @@ struct AnchorArgs {
   float* out_peak;         // [B] or NULL
   const int* path;         // draft trees: [B][path_stride] accepted nodes (NULL: linear)
   int path_stride;
+  // 1: the scores were kept by the anchor layer's cross-attention, per block row:
+  // score [rows][H][score_ld], stats [rows][H] (max, sum); only the pick kernel runs
+  int fused, score_ld;
+  unsigned long long* best;   // fused: [B] merged (weight bits, ~frame), 0 between steps
 };
-size_t anchor_score_floats(int B, int H, int max_frames);     // the scores' part
+// scratch of the readout for B sequences and `rows` block rows: the scores' part, then
+// scores + statistics (either layout)
+size_t anchor_score_floats(int rows, int B, int H, int max_frames);
+int anchor_score_ld(int max_frames);
 // The AnchorDraft training objective over B sequences of R padded rows (row t of
 // sequence b is b * R + t; M = B * R).
 struct LossArgs {
@@ -197,7 +210,7 @@ struct LossArgs {
 };
 int loss_chunks(int max_frames);
 void launch_anchordraft_loss(const LossArgs& a, hipStream_t st);
-size_t anchor_scratch_floats(int B, int H, int max_frames);   // scores + statistics
+size_t anchor_scratch_floats(int rows, int B, int H, int max_frames);
 template <class S>
 void launch_anchor(const AnchorArgs& a, int B, hipStream_t st);
 

@@ -119,11 +119,11 @@ __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, 
 // chain).  Keys a query must not see get probability 0 and value slots past k_end are
 // zeroed (stale or poisoned cache slots never reach the output).  Unmasked blocks skip
 // all of that.  Queries past the group (zero rows) are computed but never stored.
-template <bool MASKED>
+template <bool MASKED, bool SCORES = false>
 __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int n0,
                                              unsigned long long tm, int grp, const bf16x8 (&qh)[2],
                                              const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
-                                             float& l_run) {
+                                             float& l_run, float* srow = nullptr) {
   float sv[8];
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
@@ -139,6 +139,12 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
       const bool see = key >= k_lo && key < k_end && (key < n0 || ((tm >> ((key - n0) & 63)) & 1));
       sv[tt * 4 + i] = (!MASKED || see) ? st[i] : -INFINITY;
     }
+  }
+  // the anchor layer keeps every score of its query rows (keys past the sequence hold
+  // -inf; the row stride covers whole 32-key blocks; a block past the chunk stores none)
+  if (SCORES && srow && blk < k_end) {
+    *(float4*)(srow + blk + grp * 8) = float4{sv[0], sv[1], sv[2], sv[3]};
+    *(float4*)(srow + blk + grp * 8 + 4) = float4{sv[4], sv[5], sv[6], sv[7]};
   }
   const float bm = rows4_max(fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
                                    fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7]))));
@@ -220,7 +226,7 @@ __device__ __forceinline__ float4 finish_proj4(const AttnArgs& a, int m, int col
   return v;
 }
 
-template <bool CROSS>
+template <bool CROSS, bool SCORES>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(3)))
 attn_mfma_kernel(AttnArgs a) {
   extern __shared__ float part[];  // [waves][kAttnPart], then the queries [16][64]
@@ -231,6 +237,7 @@ attn_mfma_kernel(AttnArgs a) {
   const int q0 = qg * 16;
   const int nq = min(16, s.k + 1 - q0);
   if (nq <= 0) return;
+  if (SCORES && a.best_clear && h == 0 && qg == 0 && threadIdx.x == 0) a.best_clear[b] = 0;
   // cross-attention sees frames [wlo, whi) (all frames unless a window was given)
   const int n_keys = CROSS ? s.whi : s.n + q0 + nq;
   const int k_lo = CROSS ? s.wlo : 0;
@@ -363,6 +370,9 @@ attn_mfma_kernel(AttnArgs a) {
   if (active) {
     // committed keys all visible; the block's rows through the lane's row mask
     const int n0 = CROSS ? s.T : s.n;
+    // the anchor layer: this lane's query row's scores (rows past the group store none)
+    float* srow = (SCORES && c16 < nq) ? a.score_out + ((size_t)(s.row0 + q0 + c16) * a.H + h) * a.score_ld
+                                       : nullptr;
     // Q^T operand: query c16, dims 16 grp + 8 hh + j, scaled by 1/8 (exact)
     bf16x8 qh[2], ql[2];
     {
@@ -386,9 +396,9 @@ attn_mfma_kernel(AttnArgs a) {
       const int clean = CROSS ? k_end : min(k_end, s.n);
       auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
         if (blk + 32 <= clean && blk >= k_lo) {
-          attend_block<false>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run);
+          attend_block<false, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run, srow);
         } else if (CROSS) {
-          attend_block<true>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run);
+          attend_block<true, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run, srow);
         } else {
           attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
                              n0, tmask, grp, qh, ql, o, m_run, l_run);
@@ -430,6 +440,7 @@ attn_mfma_kernel(AttnArgs a) {
       acc += wgt * Q[32 + dd * 16 + qq];
     }
     afrag_store(a.out, a.out_RT, s.row0 + q0 + qq, h * kHead + dd, acc / L);
+    if (SCORES && dd == 0) a.stat_out[(size_t)(s.row0 + q0 + qq) * a.H + h] = float2{M, L};
   }
 }
 
@@ -437,8 +448,9 @@ void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st) {
   const dim3 grid(a.H, B * a.qgroups), block(64 * a.max_chunks);
   const size_t lds = ((size_t)a.max_chunks * kAttnPart + 16 * kHead) * sizeof(float) +
                      (a.cross ? 0 : 2 * kMaxBlockRows * kHead * sizeof(uint16_t));
-  if (a.cross) hipLaunchKernelGGL(attn_mfma_kernel<true>, grid, block, lds, st, a);
-  else hipLaunchKernelGGL(attn_mfma_kernel<false>, grid, block, lds, st, a);
+  if (a.cross && a.score_out) hipLaunchKernelGGL((attn_mfma_kernel<true, true>), grid, block, lds, st, a);
+  else if (a.cross) hipLaunchKernelGGL((attn_mfma_kernel<true, false>), grid, block, lds, st, a);
+  else hipLaunchKernelGGL((attn_mfma_kernel<false, false>), grid, block, lds, st, a);
 }
 
 }  // namespace ad
