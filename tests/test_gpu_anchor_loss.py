@@ -10,6 +10,9 @@ appendix "Training Correction with AnchorDraft" (eq. anchordraft-supp).
 * End to end: the draft block's forward over a block of training positions on the GPU
   (its first layer's query rows from ad_step.out_xq, its logits and features) against
   the oracle's forward of the same block.
+* The bench's launch configuration (large-v3-shape draft, 12 x 128 positions, 1500
+  frames): the token and feature terms over every row, every row of two sampled
+  utterances, sampled logit-gradient rows.
 
 Tolerances.  The keys are the draft's bf16 projection of the encoder states on both
 sides; the GPU's fp32 accumulation can put a few keys one bf16 ulp away from the
@@ -189,3 +192,57 @@ def test_end_to_end_draft_forward_and_objective():
     err = np.max(np.abs(got["dxq"] - dx)) / np.max(np.abs(dx))
     print(f"  query gradient error {err:.2e} of max")
     assert err <= 1e-3
+
+
+def test_full_size_objective_sampled_against_oracle():
+    """The bench's launch configuration: the large-v3-shape draft block (d 1280, 20 heads,
+    vocab 51866), 12 utterances x 128 positions, 1500 frames.  The oracle checks every
+    row of two sampled utterances (row cross-entropy, query gradient), the token and
+    feature terms over all rows, and sampled logit-gradient rows; the alignment term is
+    checked as the mean of the GPU's own row values, which the oracle checks row by row."""
+    from paper_2608_12703_amd.configs import CONFIGS
+    cfg = CONFIGS["large_v3_bf16"]
+    params = synth.make_params(cfg.with_(n_layers=1))      # the token and position tables
+    dparams = synth.make_draft_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    B, R = 12, 128
+    Ts = [int(t) for t in wl.T[:B]]
+    dcfg, sess = _draft_session(cfg, params, dparams, B, R, Ts)
+    encs = [synth.make_encoder(cfg, b, T) for b, T in enumerate(Ts)]
+    sess.prefill_encoder(encs)
+    g = np.random.default_rng(31)
+    M, d, V = B * R, cfg.d_model, cfg.vocab
+    xq = (g.standard_normal((M, d)) * 8).astype(np.float32)
+    center, targets, logits, feat, feat_target = _inputs(cfg, B, R, Ts, 32)
+    got = _run_loss(sess, B, R, xq, center, logits, targets, feat, feat_target)
+    assert got["err"][0] == 0
+    # token and feature terms over every row; the total's weights
+    tok, dz = al.token_loss(logits, targets)
+    feat_l, _ = al.feature_loss(feat, feat_target, targets >= 0)
+    np.testing.assert_allclose(got["terms"][1], tok, rtol=2e-5)
+    np.testing.assert_allclose(got["terms"][2], feat_l, rtol=2e-5)
+    n_valid = int(np.sum(center >= 0))
+    np.testing.assert_allclose(got["terms"][3], np.sum(got["row"].astype(np.float64)) / n_valid, rtol=1e-5)
+    np.testing.assert_allclose(got["terms"][0], got["terms"][1] + 0.5 * got["terms"][2] + LAM * got["terms"][3],
+                               rtol=1e-6)
+    rows = g.choice(M, 24, replace=False)
+    e = np.max(np.abs(got["dlogits"][rows] - dz[rows]))
+    assert e <= 1e-5 * np.max(np.abs(dz[rows])), e
+    # every row of two utterances against the oracle's alignment term
+    bm = odr.block_model(dcfg, params, dparams)
+    for b in (0, 7):
+        K = od.cross_kv(bm, encs[b])[0][0]
+        sl = slice(b * R, (b + 1) * R)
+        ref = al.anchor_loss([xq[sl].astype(np.float64)], [K], [Ts[b]], [center[sl]], SIGMA, LAM)
+        np.testing.assert_allclose(got["row"][sl], ref.row_loss[0], rtol=2e-5, atol=1e-6)
+        dx = ref.dxq[0] * (ref.n_valid / n_valid)            # the batch's |V|
+        # Per (row, head): the keys are the bf16 rounding of a 1280-term sum, taken in
+        # float32 on the GPU and float64 in the oracle, so a few sit one bf16 ulp apart
+        # (2^-8 of the key).  A head whose gradient is dominated by such a key is off by
+        # up to that fraction; every other head stays at the 16-bit operands' ~1e-5.
+        # Bound: 5e-4 of the largest entry for 99% of (row, head) pairs, 5e-3 for all.
+        err = np.abs(got["dxq"][sl] - dx).reshape(R, cfg.n_heads, 64).max(axis=2) / np.max(np.abs(dx))
+        frac = float(np.mean(err > 5e-4))
+        print(f"  utterance {b}: row losses within 2e-5; query gradient: max error {err.max():.2e} of "
+              f"max, {frac:.4f} of (row, head) pairs past 5e-4")
+        assert frac <= 0.01 and err.max() <= 5e-3
