@@ -13,6 +13,9 @@ ad_kv_commit_tree moves the accepted path's keys / values to slots n .. n + a.
   work, checked bit-exact.
 * Lossless decoding with trees (including a decoy sibling that shadows the right one)
   against autoregressive decoding on the GPU.
+* Bad parents, and the packed layout against the padded one.
+* The bench's tree step at the large-v3 shape (the 11-node tree at all 32 sequences),
+  one planted sequence against the oracle.
 """
 import numpy as np
 import pytest
@@ -267,3 +270,59 @@ def test_bad_parents_skip_only_their_sequence_and_packed_trees_agree():
         np.testing.assert_array_equal(r["logits"][rows].view(np.uint32),
                                       rp["logits"][[rowp[sum(len(t) for t in trees[:b]) + i]
                                                     for i in range(len(trees[b]))]].view(np.uint32))
+
+
+def test_large_v3_tree_step_sampled():
+    """The bench's tree step (the 11-node tree at every sequence of the large-v3 batch,
+    anchor at three quarters of the depth) with one sequence planted and checked against
+    the oracle's tree pass: node logits, greedy tokens, the walk, the anchor, the written
+    cache of every layer, and the commit's moves."""
+    from paper_2608_12703_amd.configs import CONFIGS
+    cfg = CONFIGS["large_v3_bf16"]
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    b_s = int(np.argmax(wl.n))
+    n = int(wl.n[b_s])
+    st = oracle_state(cfg, model, b_s, n, int(wl.T[b_s]), int(wl.t0[b_s]))
+    y, _, _ = od.ar_decode(model, st, 3)
+    blocks = []
+    for b in range(wl.batch):
+        fill = list(wl.fill_any[b]) * 2
+        tok = [int(wl.t0[b])] + [int(t) for t in fill[: len(TREE) - 1]]
+        if b == b_s:
+            for j, u in enumerate((1, 4, 7)):        # the greedy continuation along 0-1-4-7
+                tok[u] = y[j]
+        blocks.append(np.array(tok, np.int64))
+    layer = 3 * cfg.n_layers // 4
+    sess = device_session(cfg, params, wl, k_max=len(TREE) - 1)
+    sess.anchor_layer = layer
+    sess.step(blocks, parents=[TREE] * wl.batch)
+    res = sess.results()
+    assert res["err"] == 0
+    kv_pre = sess.export_prefix(b_s, n + len(TREE))
+    sess.commit()
+    res_c = sess.results()
+    out = od.forward_block(model, st, blocks[b_s], parents=TREE, probe_layer=layer)
+    ref = od.verify_tree(model, st, blocks[b_s], TREE)
+    rows = [sess.row_of(b_s, i) for i in range(len(TREE))]
+    err = float(np.max(np.abs(res["logits"][rows] - out.logits)))
+    print(f"  seq {b_s}: n={n}, path {ref.path}, gpu path "
+          f"{res['path'][b_s][: int(res['accept_len'][b_s]) + 1].tolist()}, logit error {err:.2e}")
+    assert err <= LOGIT_TOL["bf16"]
+    for i in range(len(TREE)):
+        if ref.margins[i] >= MARGIN_EXCLUDE:
+            assert res["greedy"][rows[i]] == ref.greedy[i]
+    for lay, (kb, vb) in enumerate(out.new_kv):
+        kv_close(kv_pre[lay, 0, n:], kb, f"layer {lay} K", "bf16")
+        kv_close(kv_pre[lay, 1, n:], vb, f"layer {lay} V", "bf16")
+    assert all(ref.margins[u] >= MARGIN_EXCLUDE for u in ref.path)
+    a = int(res["accept_len"][b_s])
+    path = res["path"][b_s][: a + 1].tolist()
+    assert path == ref.path and a == ref.accepted >= 3
+    assert res["out_tokens"][b_s][: a + 1].tolist() == ref.emitted
+    compare_anchor(cfg, res, b_s, ref, od.anchor_of(out.xattn[ref.path[-1]]))
+    kv_post = sess.export_prefix(b_s, n + a + 1)
+    np.testing.assert_array_equal(kv_post[:, :, n:].view(np.uint32),
+                                  kv_pre[:, :, [n + u for u in path]].view(np.uint32))
+    assert int(res_c["kv_len"][b_s]) == n + a + 1
