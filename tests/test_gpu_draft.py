@@ -5,7 +5,7 @@ draft from four target representations and the token embedding, one causal block
 audio cross-attention), appendix "Window geometry" (+-400 ms around the anchor).  The
 target step runs with the verification-attention anchor readout and three residual
 taps; the draft round's every input on the oracle side comes from the oracle's own
-target pass.
+target pass.  The last test runs the bench's draft step at the large-v3 shape.
 """
 import numpy as np
 import pytest
@@ -138,3 +138,43 @@ def test_speculative_decode_with_draft_equals_autoregressive():
                                                          ANCHOR_LAYER)
     print(f"[draft loop] {rounds} rounds, accepts {[a.tolist() for a in acc]}")
     assert got == toks
+
+
+def test_large_v3_draft_round_sampled():
+    """The bench's draft step: the large-v3 target step at batch 32 with the anchor at
+    three quarters of the depth and the three taps, then a round of the one-layer draft
+    block (d_ffn 2560, +-20-frame window); one sequence planted and checked against the
+    oracle's target pass and draft round."""
+    from paper_2608_12703_amd.configs import CONFIGS
+    cfg = CONFIGS["large_v3_bf16"]
+    params = synth.make_params(cfg)
+    dparams = synth.make_draft_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    b_s = int(np.argmin(wl.n))
+    blocks, _ = planted_blocks(cfg, model, wl, {b_s})
+    layer = 3 * cfg.n_layers // 4
+    sess = device_session(cfg, params, wl)
+    sess.anchor_layer = layer
+    sess.tap_layers = tuple(odr.tap_layers(cfg.n_layers))
+    sess.out_taps = torch.empty(3, sess.max_rows, cfg.d_model, dtype=torch.float32, device="cuda")
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    runner = decode.DraftRunner(sess, dparams)
+    runner.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+    got = runner.round(K).cpu().numpy()
+    st = oracle_state(cfg, model, b_s, int(wl.n[b_s]), int(wl.T[b_s]), int(wl.t0[b_s]))
+    ref, anc = od.verify_with_anchor(model, st, blocks[b_s][1:], layer)
+    a = ref.accepted
+    assert int(res["accept_len"][b_s]) == a and int(res["anchor"][b_s]) == anc.frame
+    out = od.forward_block(model, st, blocks[b_s], taps=odr.tap_layers(cfg.n_layers))
+    bm = odr.block_model(synth.draft_config(cfg), params, dparams)
+    dcross = od.cross_kv(bm, synth.make_encoder(cfg, b_s, int(wl.T[b_s])))
+    want = odr.draft_round(bm, dparams, dcross, out.taps[:, a], out.hidden[a], ref.greedy[a],
+                           anc.frame, int(wl.T[b_s]), K)
+    cut = next((j for j, m in enumerate(want.margins) if m < MARGIN_EXCLUDE), K)
+    print(f"  seq {b_s}: a={a} anchor={anc.frame} drafts gpu {got[b_s].tolist()} oracle {want.drafts} "
+          f"(compared {cut}), margins {np.round(want.margins, 4).tolist()}")
+    assert got[b_s][:cut].tolist() == want.drafts[:cut]
+    assert cut >= 1
