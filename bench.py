@@ -400,6 +400,17 @@ def main():
         cpu = cpu_baseline(cfg, params, wl)
         log(f"oracle: {cpu['value']:.3f} tokens/s")
 
+    # The paper's break-even rule for the runtime correction (section "Correction and
+    # Cost"): a round of K draft steps costs about 1 + K rho verify steps; reading the
+    # anchor adds Delta C_corr, which pays when the accepted length grows by at least
+    # Delta L / (1 + L) >= Delta C_corr / (1 + K rho).
+    break_even = None
+    if anchor is not None and draft is not None:
+        dc = max(anchor["us_per_step_delta"], 0.0) / (ms * 1e3)
+        K = draft["draft_steps_per_round"]
+        break_even = {"K": K, "rho": draft["rho"], "delta_c_corr": round(dc, 5),
+                      "min_relative_length_gain": round(dc / (1 + K * draft["rho"]), 5)}
+
     out = {
         "metric": "accepted tokens/s, large-v3-shape spec-verify step (bf16); % of HBM roofline",
         "value": round(tokens / (ms / 1e3), 1),
@@ -419,6 +430,7 @@ def main():
         "draft_step": draft,
         "tree_step": tree,
         "anchordraft_loss": loss,
+        "break_even": break_even,
     }
     print(json.dumps(out), flush=True)
 
