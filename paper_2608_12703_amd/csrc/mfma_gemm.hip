@@ -437,12 +437,16 @@ int gemm_splits(int N, int K) {
 // ones in one round (a K step of 8 row tiles costs 0.43 us against 0.27 us): the 352-row
 // block of an 11-node tree at batch 32 takes 6.16 ms per step against 6.58 ms.  The
 // row tiling never changes a row's sums (same K order, same split order).
+// When no tile fits (the LM head's 406 column tiles), 16 row tiles, or 4 when that
+// needs no more row chunks (up to 64 rows, the draft block's 32): a 4-row-tile K step
+// costs a third of a 16-row-tile one (draft step 198 -> 156 us at batch 32).  For the
+// 352-row tree block 8 row tiles measured slower than 16 (6.20 against 6.16 ms).
 constexpr int kMaxWGsRows = 384;
 int gemm_rtc(int M, int N, int S) {
   const int ntiles = (N + kNT - 1) / kNT;
   for (int rtc : {4, 8})
     if (ntiles * mchunks_of(M, rtc) * S <= kMaxWGsRows) return rtc;
-  return 16;
+  return mchunks_of(M, 4) == mchunks_of(M, 16) ? 4 : 16;
 }
 
 size_t gemm_part_floats(int M, int N, int K) { return (size_t)gemm_splits(N, K) * M * N; }
