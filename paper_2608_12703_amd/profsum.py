@@ -3,6 +3,9 @@
   python -m paper_2608_12703_amd.profsum kernels RESULTS.db [--calls N] [--command CMD]
       per-kernel dispatch count, mean / min / max duration and share of GPU time
       (--calls: divide the totals by this many verify steps)
+  python -m paper_2608_12703_amd.profsum step RESULTS.db --marker NAME [--which I]
+      the kernels of one step: from the I-th dispatch whose name contains NAME to the
+      next one (negative I counts from the end)
   python -m paper_2608_12703_amd.profsum traffic --fetch FETCH.db --write WRITE.db
           --kernel NAME --calib-mib MIB --out OUT.json [--command CMD]
       HBM bytes per dispatch of one kernel from a FETCH_SIZE run and a WRITE_SIZE run,
@@ -31,6 +34,29 @@ def kernel_table(db: str, calls: int | None = None) -> str:
         if calls:
             line += f" {tot / 1e3 / calls:9.1f}"
         out.append(line)
+    return "\n".join(out)
+
+
+def step_table(db: str, marker: str, which: int) -> str:
+    """Kernels of one step: the dispatches from the `which`-th dispatch whose name contains
+    `marker` (negative counts from the end) up to the next one, summed per kernel name
+    in order of first appearance."""
+    cur = sqlite3.connect(db).cursor()
+    rows = cur.execute("select name, start, end from kernels order by start").fetchall()
+    idx = [i for i, r in enumerate(rows) if marker in r[0]]
+    i0 = idx[which]
+    nxt = [i for i in idx if i > i0]
+    i1 = nxt[0] if nxt else len(rows)
+    agg = {}
+    for name, st, en in rows[i0:i1]:
+        e = agg.setdefault(name, [0.0, 0])
+        e[0] += (en - st) / 1e3
+        e[1] += 1
+    total = sum(v[0] for v in agg.values())
+    out = [f"{'kernel':70s} {'calls':>6s} {'us':>9s} {'share':>6s}"]
+    for name, (us, n) in agg.items():
+        out.append(f"{name[:70]:70s} {n:6d} {us:9.1f} {100 * us / total:5.1f}%")
+    out.append(f"{'sum of kernel durations':70s} {'':6s} {total:9.1f}")
     return "\n".join(out)
 
 
@@ -66,6 +92,10 @@ def main(argv=None):
     k.add_argument("db")
     k.add_argument("--calls", type=int)
     k.add_argument("--command", default="")
+    st = sub.add_parser("step")
+    st.add_argument("db")
+    st.add_argument("--marker", required=True)
+    st.add_argument("--which", type=int, default=-2)
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -78,6 +108,8 @@ def main(argv=None):
         if a.command:
             print(f"command: {a.command}\n")
         print(kernel_table(a.db, a.calls))
+    elif a.cmd == "step":
+        print(step_table(a.db, a.marker, a.which))
     else:
         rec = traffic(a.fetch, a.write, a.kernel, a.calib_mib, a.command)
         with open(a.out, "w") as fh:
