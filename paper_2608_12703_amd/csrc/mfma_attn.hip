@@ -62,27 +62,40 @@ struct KVTiles {
 // Load the 32-key block starting at blk (a multiple of 32 from the chunk start).  A
 // 16-key tile past k_end is replaced by the chunk's last tile (valid, and just read, so
 // the reload hits the cache), so every lane issues the same unconditional loads.
+// Cross-attention: this lane's first key element of the 32-frame block starting at blk
+// (keys and values already in operand order, 1 KB per load; the block's values follow
+// its keys).  A block past the chunk is replaced by the chunk's last block, and a chunk
+// wholly before a cross-attention window (k_end <= k_beg) reloads its first block, which
+// lies inside the sequence's slots.
+__device__ __forceinline__ const uint16_t* cross_block(const AttnArgs& a, const SeqDesc& s, int h,
+                                                      int blk, int k_beg, int k_end, int c16, int grp) {
+  const int b0 = blk < k_end ? blk
+                             : (k_end > k_beg ? k_beg + (k_end - 1 - k_beg) / kCrossBlock * kCrossBlock : k_beg);
+  const size_t bo = (size_t)((s.enc_off + b0) / kCrossBlock) * 2 * kCrossBlockElems + (grp * 16 + c16) * 8;
+  return a.kv + cross_base(a.layer, h, a.H, a.frames_cap) + bo;
+}
+__device__ __forceinline__ void load_keys(const uint16_t* kp, KVTiles& t) {
+  t.k00 = *(const uint4*)(kp + 0 * 512);
+  t.k01 = *(const uint4*)(kp + 1 * 512);
+  t.k10 = *(const uint4*)(kp + 2 * 512);
+  t.k11 = *(const uint4*)(kp + 3 * 512);
+}
+__device__ __forceinline__ void load_values(const uint16_t* kp, KVTiles& t) {
+  const uint16_t* vp = kp + kCrossBlockElems;
+  t.v0 = *(const uint4*)(vp + 0 * 512);
+  t.v1 = *(const uint4*)(vp + 1 * 512);
+  t.v2 = *(const uint4*)(vp + 2 * 512);
+  t.v3 = *(const uint4*)(vp + 3 * 512);
+}
+
 template <bool CROSS>
 __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, int h, int blk,
                                            int k_beg, int k_end, int pg_lane, int c16, int grp,
                                            KVTiles& t) {
   if (CROSS) {
-    // one 32-frame block: keys and values already in operand order, 1 KB per load
-    // (a chunk wholly before a cross-attention window has k_end <= k_beg: it reloads its
-    // first block, which lies inside the sequence's slots)
-    const int b0 = blk < k_end ? blk
-                               : (k_end > k_beg ? k_beg + (k_end - 1 - k_beg) / kCrossBlock * kCrossBlock : k_beg);
-    const size_t bo = (size_t)((s.enc_off + b0) / kCrossBlock) * 2 * kCrossBlockElems + (grp * 16 + c16) * 8;
-    const uint16_t* kp = a.kv + cross_base(a.layer, h, a.H, a.frames_cap) + bo;
-    const uint16_t* vp = kp + kCrossBlockElems;
-    t.k00 = *(const uint4*)(kp + 0 * 512);
-    t.k01 = *(const uint4*)(kp + 1 * 512);
-    t.k10 = *(const uint4*)(kp + 2 * 512);
-    t.k11 = *(const uint4*)(kp + 3 * 512);
-    t.v0 = *(const uint4*)(vp + 0 * 512);
-    t.v1 = *(const uint4*)(vp + 1 * 512);
-    t.v2 = *(const uint4*)(vp + 2 * 512);
-    t.v3 = *(const uint4*)(vp + 3 * 512);
+    const uint16_t* kp = cross_block(a, s, h, blk, k_beg, k_end, c16, grp);
+    load_keys(kp, t);
+    load_values(kp, t);
     return;
   }
   const uint16_t* kb[2];
@@ -119,12 +132,12 @@ __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, 
 // chain).  Keys a query must not see get probability 0 and value slots past k_end are
 // zeroed (stale or poisoned cache slots never reach the output).  Unmasked blocks skip
 // all of that.  Queries past the group (zero rows) are computed but never stored.
+// The block's scores (this lane's query, keys 8 grp .. 8 grp + 7), masked keys -inf.
 template <bool MASKED, bool SCORES = false>
-__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int n0,
+__device__ __forceinline__ void block_scores(const KVTiles& cur, int blk, int k_lo, int k_end, int n0,
                                              unsigned long long tm, int grp, const bf16x8 (&qh)[2],
-                                             const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
-                                             float& l_run, float* srow = nullptr) {
-  float sv[8];
+                                             const bf16x8 (&ql)[2], float (&sv)[8],
+                                             float* srow = nullptr) {
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -146,6 +159,13 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
     *(float4*)(srow + blk + grp * 8) = float4{sv[0], sv[1], sv[2], sv[3]};
     *(float4*)(srow + blk + grp * 8 + 4) = float4{sv[4], sv[5], sv[6], sv[7]};
   }
+}
+
+// The online-softmax update with the block's scores and the value product.
+template <bool MASKED>
+__device__ __forceinline__ void block_softmax_pv(const KVTiles& cur, const float (&sv)[8], int blk,
+                                                 int k_end, int grp, f32x4 (&o)[4], float& m_run,
+                                                 float& l_run) {
   const float bm = rows4_max(fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
                                    fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7]))));
   const float m_new = fmaxf(m_run, bm);
@@ -173,6 +193,16 @@ __device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_
     o[dt] = mfma_bf16(vt, ph, o[dt]);
     o[dt] = mfma_bf16(vt, pl, o[dt]);
   }
+}
+
+template <bool MASKED, bool SCORES = false>
+__device__ __forceinline__ void attend_block(const KVTiles& cur, int blk, int k_lo, int k_end, int n0,
+                                             unsigned long long tm, int grp, const bf16x8 (&qh)[2],
+                                             const bf16x8 (&ql)[2], f32x4 (&o)[4], float& m_run,
+                                             float& l_run, float* srow = nullptr) {
+  float sv[8];
+  block_scores<MASKED, SCORES>(cur, blk, k_lo, k_end, n0, tm, grp, qh, ql, sv, srow);
+  block_softmax_pv<MASKED>(cur, sv, blk, k_end, grp, o, m_run, l_run);
 }
 
 // Self-attention: replace the keys / values of the block's own rows (positions n ..
@@ -404,11 +434,35 @@ attn_mfma_kernel(AttnArgs a) {
                              n0, tmask, grp, qh, ql, o, m_run, l_run);
         }
       };
-      for (int blk = k_beg; blk < k_end; blk += 64) {
-        attend(ta, blk);
-        load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
-        attend(tb, blk + 32);
-        load_block<CROSS>(a, s, h, blk + 96, k_beg, k_end, pg_lane, c16, grp, tb);
+      if constexpr (CROSS) {
+        // a block's key registers are free once its scores are in: the keys of the block
+        // two ahead are requested then, and its values after the value product, so more
+        // bytes stay in flight while the softmax runs
+        auto step = [&](KVTiles& t, int blk) __attribute__((always_inline)) {
+          const uint16_t* np = cross_block(a, s, h, blk + 64, k_beg, k_end, c16, grp);
+          float sv[8];
+          if (blk + 32 <= clean && blk >= k_lo) {
+            block_scores<false, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, sv, srow);
+            load_keys(np, t);
+            block_softmax_pv<false>(t, sv, blk, k_end, grp, o, m_run, l_run);
+          } else {
+            block_scores<true, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, sv, srow);
+            load_keys(np, t);
+            block_softmax_pv<true>(t, sv, blk, k_end, grp, o, m_run, l_run);
+          }
+          load_values(np, t);
+        };
+        for (int blk = k_beg; blk < k_end; blk += 64) {
+          step(ta, blk);
+          step(tb, blk + 32);
+        }
+      } else {
+        for (int blk = k_beg; blk < k_end; blk += 64) {
+          attend(ta, blk);
+          load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
+          attend(tb, blk + 32);
+          load_block<CROSS>(a, s, h, blk + 96, k_beg, k_end, pg_lane, c16, grp, tb);
+        }
       }
     }
     if (grp == 0) {
