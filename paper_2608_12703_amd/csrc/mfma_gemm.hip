@@ -9,7 +9,8 @@
 // a register ring five steps ahead for tiles of up to 8 row tiles (the A-fragment order
 // is the matrix instruction's lane order, so each is one coalesced 16-byte load per
 // lane; keeping them out of LDS removes a third of the step's LDS traffic), and through
-// a three-stage LDS ring for 16 row tiles.  The waits are explicit; the loop is unrolled
+// a three-stage LDS ring for 16 row tiles.  Workgroups with long K ranges (the FFN
+// products) take two K steps per barrier.  The waits are explicit; the loops are unrolled
 // over the ring stages so every buffer is a distinct object.  Small-N products split K over several
 // workgroups and the last one to finish a tile sums the partial tiles in split order.
 // The split count depends on the weight shape only, so a row's result never depends
@@ -132,7 +133,7 @@ __device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RTC / 4][4], const AFr
   }
 }
 
-template <int EPI, int RTC, bool PACKED>
+template <int EPI, int RTC, bool PACKED, bool TWO = false>
 __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   constexpr int RW = RTC / 4;            // row tiles per wave
   constexpr int NA = RTC / 4;            // direct loads per wave for one activation stage
@@ -203,40 +204,78 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
       }
     };
     AFrag<RW> a0, a1, a2, a3, a4, a5;
-    la(a0, kb0);
-    iw(sw0, kb0);
-    la(a1, kb0 + 1);
-    iw(sw1, kb0 + 1);
-    la(a2, kb0 + 2);
-    iw(sw2, kb0 + 2);
-    la(a3, kb0 + 3);
-    iw(sw3, kb0 + 3);
-    la(a4, kb0 + 4);
-    iw(sw4, kb0 + 4);
-    BARRIER_VMCNT(kWait);
-#define GEMM_STEP(CA, CW, NXA, NXW)                 \
-  {                                                 \
-    la(NXA, kb + 5);                                \
-    iw(NXW, kb + 5);                                \
-    mma_step_reg<RTC>(acc, CA, CW, ch, lane);       \
-    BARRIER_VMCNT(kWait);                           \
-    ++kb;                                           \
-  }
-    for (int it = 0; it < nk / 6; ++it) {
-      GEMM_STEP(a0, sw0, a5, sw5)
-      GEMM_STEP(a1, sw1, a0, sw0)
-      GEMM_STEP(a2, sw2, a1, sw1)
-      GEMM_STEP(a3, sw3, a2, sw2)
-      GEMM_STEP(a4, sw4, a3, sw3)
-      GEMM_STEP(a5, sw5, a4, sw4)
+    if constexpr (TWO) {
+      // Long K ranges (TWO) take two K steps per barrier: iteration i (steps 2i, 2i + 1)
+      // requests A and W of steps 2i + 4 and 2i + 5, multiplies, and ends with the
+      // previous iteration's loads complete.  (Short ranges keep one step per barrier:
+      // the first wait then covers one stage instead of two.)
+      constexpr int kWait2 = 2 * (kA + 1);
+      la(a0, kb0);
+      iw(sw0, kb0);
+      la(a1, kb0 + 1);
+      iw(sw1, kb0 + 1);
+      la(a2, kb0 + 2);
+      iw(sw2, kb0 + 2);
+      la(a3, kb0 + 3);
+      iw(sw3, kb0 + 3);
+      BARRIER_VMCNT(kWait2);
+#define GEMM_ITER(CA0, CW0, CA1, CW1, NA0, NW0, NA1, NW1)         \
+    {                                                             \
+      la(NA0, kb + 4);                                            \
+      iw(NW0, kb + 4);                                            \
+      la(NA1, kb + 5);                                            \
+      iw(NW1, kb + 5);                                            \
+      mma_step_reg<RTC>(acc, CA0, CW0, ch, lane);                 \
+      if (kb + 1 < kb1) mma_step_reg<RTC>(acc, CA1, CW1, ch, lane);\
+      BARRIER_VMCNT(kWait2);                                      \
+      kb += 2;                                                    \
     }
-    const int rem = nk % 6;
-    if (rem >= 1) GEMM_STEP(a0, sw0, a5, sw5)
-    if (rem >= 2) GEMM_STEP(a1, sw1, a0, sw0)
-    if (rem >= 3) GEMM_STEP(a2, sw2, a1, sw1)
-    if (rem >= 4) GEMM_STEP(a3, sw3, a2, sw2)
-    if (rem >= 5) GEMM_STEP(a4, sw4, a3, sw3)
+      const int iters = (nk + 1) >> 1;
+      for (int it = 0; it < iters / 3; ++it) {
+        GEMM_ITER(a0, sw0, a1, sw1, a4, sw4, a5, sw5)
+        GEMM_ITER(a2, sw2, a3, sw3, a0, sw0, a1, sw1)
+        GEMM_ITER(a4, sw4, a5, sw5, a2, sw2, a3, sw3)
+      }
+      const int rem = iters % 3;
+      if (rem >= 1) GEMM_ITER(a0, sw0, a1, sw1, a4, sw4, a5, sw5)
+      if (rem >= 2) GEMM_ITER(a2, sw2, a3, sw3, a0, sw0, a1, sw1)
+#undef GEMM_ITER
+    } else {
+      la(a0, kb0);
+      iw(sw0, kb0);
+      la(a1, kb0 + 1);
+      iw(sw1, kb0 + 1);
+      la(a2, kb0 + 2);
+      iw(sw2, kb0 + 2);
+      la(a3, kb0 + 3);
+      iw(sw3, kb0 + 3);
+      la(a4, kb0 + 4);
+      iw(sw4, kb0 + 4);
+      BARRIER_VMCNT(kWait);
+#define GEMM_STEP(CA, CW, NXA, NXW)                 \
+    {                                               \
+      la(NXA, kb + 5);                              \
+      iw(NXW, kb + 5);                              \
+      mma_step_reg<RTC>(acc, CA, CW, ch, lane);     \
+      BARRIER_VMCNT(kWait);                         \
+      ++kb;                                         \
+    }
+      for (int it = 0; it < nk / 6; ++it) {
+        GEMM_STEP(a0, sw0, a5, sw5)
+        GEMM_STEP(a1, sw1, a0, sw0)
+        GEMM_STEP(a2, sw2, a1, sw1)
+        GEMM_STEP(a3, sw3, a2, sw2)
+        GEMM_STEP(a4, sw4, a3, sw3)
+        GEMM_STEP(a5, sw5, a4, sw4)
+      }
+      const int rem = nk % 6;
+      if (rem >= 1) GEMM_STEP(a0, sw0, a5, sw5)
+      if (rem >= 2) GEMM_STEP(a1, sw1, a0, sw0)
+      if (rem >= 3) GEMM_STEP(a2, sw2, a1, sw1)
+      if (rem >= 4) GEMM_STEP(a3, sw3, a2, sw2)
+      if (rem >= 5) GEMM_STEP(a4, sw4, a3, sw3)
 #undef GEMM_STEP
+    }
   } else {
     // Step j requests activations j + 2 and weights j + 5, in that order; the prologue
     // plays virtual steps -5 .. -1 so the outstanding-load count is the same everywhere:
@@ -461,19 +500,33 @@ void launch_pack_weight(const uint16_t* W, int N, int K, uint16_t* P, hipStream_
 
 int lm_records(int V) { return 2 * ((V + kNT - 1) / kNT); }
 
+// Workgroups with at least this many K steps take two steps per barrier (FFN up and
+// down at d 1280: 40 and 26-27 steps; measured 1.7 us faster for the down-projection,
+// while the 8-step d x d products are faster with one step per barrier).  The loop
+// choice never changes the order of a tile's sums.
+constexpr int kTwoStepMin = 24;
+
+template <int EPI, int RTC, bool PACKED>
+static void launch_rtc(const GemmArgs& g, dim3 grid, hipStream_t st) {
+  if (RTC <= 8 && g.KB / g.S >= kTwoStepMin)
+    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, RTC <= 8>), grid, dim3(512), 0, st, g);
+  else
+    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, false>), grid, dim3(512), 0, st, g);
+}
+
 template <int EPI>
 static void launch_one(GemmArgs g, hipStream_t st) {
   const int rtc = gemm_rtc(g.M, g.N, g.S);
   g.mchunks = mchunks_of(g.M, rtc);
-  const dim3 grid(g.ntiles * g.S * g.mchunks), block(512);
+  const dim3 grid(g.ntiles * g.S * g.mchunks);
   if (g.packed) {
-    if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4, true>), grid, block, 0, st, g);
-    else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8, true>), grid, block, 0, st, g);
-    else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16, true>), grid, block, 0, st, g);
+    if (rtc == 4) launch_rtc<EPI, 4, true>(g, grid, st);
+    else if (rtc == 8) launch_rtc<EPI, 8, true>(g, grid, st);
+    else launch_rtc<EPI, 16, true>(g, grid, st);
   } else {
-    if (rtc == 4) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 4, false>), grid, block, 0, st, g);
-    else if (rtc == 8) hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 8, false>), grid, block, 0, st, g);
-    else hipLaunchKernelGGL((gemm_mfma_kernel<EPI, 16, false>), grid, block, 0, st, g);
+    if (rtc == 4) launch_rtc<EPI, 4, false>(g, grid, st);
+    else if (rtc == 8) launch_rtc<EPI, 8, false>(g, grid, st);
+    else launch_rtc<EPI, 16, false>(g, grid, st);
   }
 }
 
