@@ -393,7 +393,8 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   }
 
   // EPI_PARTIAL: the raw split-K partial product straight from registers (16 lanes store
-  // 64 contiguous bytes of a row); the consumer kernel sums the splits in split order.
+  // 64 contiguous bytes of a row, non-temporal: only the consumer kernel reads them); the
+  // consumer kernel sums the splits in split order.
   float* P = g.part + (size_t)s * g.M * g.N;
 #pragma unroll
   for (int r = 0; r < RW; ++r)
@@ -404,7 +405,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         const int n = col_base + ct * 16;
-        if (n < g.N) P[(size_t)m * g.N + n] = acc[r][ct][i];
+        if (n < g.N) __builtin_nontemporal_store(acc[r][ct][i], &P[(size_t)m * g.N + n]);
       }
     }
 }
