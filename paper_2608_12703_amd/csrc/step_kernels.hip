@@ -234,6 +234,16 @@ __device__ __forceinline__ void afrag_store4(uint16_t* base, int RT, int m, int 
       uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
 }
 
+// Row of workgroup `bid` for the row-per-workgroup kernels that write A-fragment
+// operands.  Workgroups are dealt round-robin over the 8 XCDs; this numbering puts the
+// 8 rows that share each 128-byte line of the output (rows 8a .. 8a + 7) on one XCD, so
+// its L2 merges their 16-byte pieces into whole lines.  Launch ceil(M / 64) * 64
+// workgroups; rows past M exit.
+__device__ __forceinline__ int xcd_row(int bid) {
+  return (bid >> 6) * 64 + (bid & 7) * 8 + ((bid >> 3) & 7);
+}
+__host__ inline int xcd_row_grid(int M) { return (M + 63) / 64 * 64; }
+
 // Residual update and the next LayerNorm of one row: x += sum_s P[s] + bias, then
 // LN(x) * g + b goes out in A-fragment order (and to `out` when given).  One thread per
 // 4 columns (blockDim = d / 4 rounded up to whole waves).
@@ -243,7 +253,8 @@ __global__ void __launch_bounds__(1024) reduce_res_ln_kernel(int M, int d, int n
                                                              const uint16_t* b, uint16_t* frag,
                                                              int RT, float* out) {
   __shared__ float red_mean[16], red_var[16];
-  const int m = blockIdx.x, j = threadIdx.x * 4;
+  const int m = xcd_row(blockIdx.x), j = threadIdx.x * 4;
+  if (m >= M) return;
   const bool on = j < d;
   const int jc = on ? j : 0;
   const size_t e = (size_t)m * d + jc;
@@ -273,7 +284,7 @@ __global__ void __launch_bounds__(1024) reduce_res_ln_kernel(int M, int d, int n
 
 // Embedding of the block rows fused with the first LayerNorm.
 template <class S>
-__global__ void __launch_bounds__(256) embed_ln_kernel(int d, const RowDesc* rows,
+__global__ void __launch_bounds__(256) embed_ln_kernel(int M, int d, const RowDesc* rows,
                                                        const typename S::T* tok_emb,
                                                        const typename S::T* pos_emb, float* x,
                                                        const float* in_rows,
@@ -282,7 +293,8 @@ __global__ void __launch_bounds__(256) embed_ln_kernel(int d, const RowDesc* row
                                                        int RT) {
   extern __shared__ float row[];
   __shared__ float red[4];
-  const int m = blockIdx.x;
+  const int m = xcd_row(blockIdx.x);
+  if (m >= M) return;
   const RowDesc r = rows[m];
   float sum = 0.f;
   for (int j = threadIdx.x; j < d; j += 256) {
@@ -556,14 +568,14 @@ void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* 
                           const void* g, const void* b, uint16_t* frag, int RT, float* out,
                           hipStream_t st) {
   const int threads = (d / 4 + kWave - 1) / kWave * kWave;
-  hipLaunchKernelGGL(reduce_res_ln_kernel, dim3(M), dim3(threads), 0, st, M, d, nsplit, P,
+  hipLaunchKernelGGL(reduce_res_ln_kernel, dim3(xcd_row_grid(M)), dim3(threads), 0, st, M, d, nsplit, P,
                      (const uint16_t*)bias, x, (const uint16_t*)g, (const uint16_t*)b, frag, RT, out);
 }
 
 void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
                      const float* in_rows, const void* g, const void* b, uint16_t* frag, int RT,
                      hipStream_t st) {
-  hipLaunchKernelGGL(embed_ln_kernel<BF16>, dim3(M), dim3(256), d * sizeof(float), st, d, rows,
+  hipLaunchKernelGGL(embed_ln_kernel<BF16>, dim3(xcd_row_grid(M)), dim3(256), d * sizeof(float), st, M, d, rows,
                      (const uint16_t*)tok, (const uint16_t*)pos, x, in_rows, (const uint16_t*)g,
                      (const uint16_t*)b, frag, RT);
 }
