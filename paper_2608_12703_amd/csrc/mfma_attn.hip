@@ -59,9 +59,6 @@ struct KVTiles {
   uint4 v0, v1, v2, v3;
 };
 
-// Load the 32-key block starting at blk (a multiple of 32 from the chunk start).  A
-// 16-key tile past k_end is replaced by the chunk's last tile (valid, and just read, so
-// the reload hits the cache), so every lane issues the same unconditional loads.
 // Cross-attention: this lane's first key element of the 32-frame block starting at blk
 // (keys and values already in operand order, 1 KB per load; the block's values follow
 // its keys).  A block past the chunk is replaced by the chunk's last block, and a chunk
@@ -88,6 +85,9 @@ __device__ __forceinline__ void load_values(const uint16_t* kp, KVTiles& t) {
   t.v3 = *(const uint4*)(vp + 3 * 512);
 }
 
+// Load the 32-key block starting at blk (a multiple of 32 from the chunk start).  A
+// 16-key tile past k_end is replaced by the chunk's last tile (valid, and just read, so
+// the reload hits the cache), so every lane issues the same unconditional loads.
 template <bool CROSS>
 __device__ __forceinline__ void load_block(const AttnArgs& a, const SeqDesc& s, int h, int blk,
                                            int k_beg, int k_end, int pg_lane, int c16, int grp,
@@ -424,16 +424,6 @@ attn_mfma_kernel(AttnArgs a) {
       // blocks below `clean` need no masking for any query of the group and (self)
       // hold committed keys only
       const int clean = CROSS ? k_end : min(k_end, s.n);
-      auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
-        if (blk + 32 <= clean && blk >= k_lo) {
-          attend_block<false, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run, srow);
-        } else if (CROSS) {
-          attend_block<true, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run, srow);
-        } else {
-          attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
-                             n0, tmask, grp, qh, ql, o, m_run, l_run);
-        }
-      };
       if constexpr (CROSS) {
         // a block's key registers are free once its scores are in: the keys of the block
         // two ahead are requested then, and its values after the value product, so more
@@ -457,6 +447,13 @@ attn_mfma_kernel(AttnArgs a) {
           step(tb, blk + 32);
         }
       } else {
+        auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
+          if (blk + 32 <= clean && blk >= k_lo)
+            attend_block<false>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, o, m_run, l_run);
+          else
+            attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
+                               n0, tmask, grp, qh, ql, o, m_run, l_run);
+        };
         for (int blk = k_beg; blk < k_end; blk += 64) {
           attend(ta, blk);
           load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
