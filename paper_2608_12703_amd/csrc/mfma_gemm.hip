@@ -502,9 +502,10 @@ void launch_pack_weight(const uint16_t* W, int N, int K, uint16_t* P, hipStream_
 int lm_records(int V) { return 2 * ((V + kNT - 1) / kNT); }
 
 // Workgroups with at least this many K steps take two steps per barrier (FFN up and
-// down at d 1280: 40 and 26-27 steps; measured 1.7 us faster for the down-projection,
-// while the 8-step d x d products are faster with one step per barrier).  The loop
-// choice never changes the order of a tile's sums.
+// down at d 1280: 40 and 26-27 steps; the down-projection measured 1.7 us faster alone
+// and 0.2-0.5 us faster inside the verify step, while the 8-step d x d products are
+// faster with one step per barrier).  The loop choice never changes the order of a
+// tile's sums.
 constexpr int kTwoStepMin = 24;
 
 template <int EPI, int RTC, bool PACKED>
