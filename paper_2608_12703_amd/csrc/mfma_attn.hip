@@ -262,6 +262,17 @@ attn_mfma_kernel(AttnArgs a) {
   extern __shared__ float part[];  // [waves][kAttnPart], then the queries [16][64]
   const int h = blockIdx.x;
   const int b = blockIdx.y / a.qgroups, qg = blockIdx.y % a.qgroups;
+  const int ch = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, c16 = lane & 15, grp = lane >> 4;
+  // self-attention: the page indices of this wave's own chunk (one per lane, lanes past
+  // the chunk's tiles repeat its first tile) do not depend on the sequence descriptor,
+  // so they are requested beside it
+  int pg_spec = 0;
+  if (!CROSS) {
+    const int tiles = a.chunk / kTile;
+    const int p = min(ch * tiles + (lane < tiles ? lane : 0), a.pages_per_seq - 1);
+    pg_spec = a.block_table[(size_t)b * a.pages_per_seq + p];
+  }
   const SeqDesc s = a.seqs[b];
   if (!s.valid) return;
   const int q0 = qg * 16;
@@ -272,26 +283,22 @@ attn_mfma_kernel(AttnArgs a) {
   const int n_keys = CROSS ? s.whi : s.n + q0 + nq;
   const int k_lo = CROSS ? s.wlo : 0;
   const int n_chunks = (n_keys + a.chunk - 1) / a.chunk;
-  const int ch = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63, c16 = lane & 15, grp = lane >> 4;
   float* Pc = part + ch * kAttnPart;
   float* qs = part + a.max_chunks * kAttnPart;
 
   const bool active = ch < n_chunks;
-  // a wave past the last chunk issues the loads of chunk 0 (valid addresses, results
-  // unused): every wave runs the same straight-line prologue, so the compiler keeps
-  // exact outstanding-load counts through it
+  // a cross-attention wave past the last chunk issues the loads of chunk 0 (valid
+  // addresses, results unused); a self-attention wave past it issues no key loads
   // the chunk's keys [k_beg, k_end); blocks before the window's first 32-key block are
   // skipped (a chunk wholly before the window streams nothing and merges with weight 0)
   const int k_end = min((active ? ch * a.chunk : 0) + a.chunk, n_keys);
   const int k_beg = max(active ? ch * a.chunk : 0, k_lo / kCrossBlock * kCrossBlock);
-  // self-attention: the chunk's page indices, one per lane (lanes past the chunk repeat
-  // its first page)
+  // self-attention: the chunk's page indices, one per lane (lanes past the chunk's last
+  // page repeat its first page; only an active wave uses them)
   int pg_lane = 0;
   if (!CROSS) {
     const int npg = (k_end - k_beg + kTile - 1) / kTile;
-    const int p = k_beg / kTile + (lane < npg ? lane : 0);
-    pg_lane = min(max(a.block_table[(size_t)b * a.pages_per_seq + p], 0), a.num_pages - 1);
+    pg_lane = min(max(__shfl(pg_spec, lane < npg ? lane : 0, kWave), 0), a.num_pages - 1);
   }
   uint16_t* nk = (uint16_t*)(qs + 16 * kHead);   // self: the block rows' keys and values
   uint16_t* nvt = nk + kMaxBlockRows * kHead;
@@ -329,8 +336,10 @@ attn_mfma_kernel(AttnArgs a) {
   asm volatile("" ::: "memory");
   // the first two key blocks
   KVTiles ta, tb;
-  load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
-  load_block<CROSS>(a, s, h, k_beg + 32, k_beg, k_end, pg_lane, c16, grp, tb);
+  if (CROSS || active) {
+    load_block<CROSS>(a, s, h, k_beg, k_beg, k_end, pg_lane, c16, grp, ta);
+    load_block<CROSS>(a, s, h, k_beg + 32, k_beg, k_end, pg_lane, c16, grp, tb);
+  }
   // split sum in split order (planes past SP, if any, in a loop), plus the bias
   auto finish = [&](const float4 (&pp)[SP], uint2 bu, size_t e) -> float4 {
     // planes past S add -0, which leaves every value (signed zeros included) unchanged;
