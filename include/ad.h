@@ -250,9 +250,9 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* step, void* strea
 
 /*
  * Input rows of the audio-conditioned draft block (paper, section 3 "Models and
- * Protocol": the draft follows EAGLE-3 and adds cross-attention to the audio encoder;
- * appendix "Draft architecture": four frozen target representations combined with the
- * current token embedding, then one causal block).  For every sequence b
+ * Protocol": an EAGLE-3 style drafter that also attends to the encoder output;
+ * appendix "Draft architecture": the input mixes four target feature vectors with the
+ * current token's embedding ahead of a single causal block).  For every sequence b
  *   out[b] = W_in [f_b ; E_tok[t_b]] + b_in                         (float32 [B][d])
  * where f_b = W_fuse [taps_0 ; taps_1 ; taps_2 ; hidden] + b_fuse at sequence b's last
  * verified row of a target step when `taps` is given (a round's first draft step; the

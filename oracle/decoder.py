@@ -241,6 +241,7 @@ class VerifyOut:
     hidden: np.ndarray    # [k+1, d]
     state: SeqState       # state after commit
     block_kv: list        # per layer (K, V) written for all k+1 block rows, [k+1, H, 64]
+    taps: np.ndarray | None = None   # residual stream after the requested layers [t, k+1, d]
 
 
 def decide(logits: np.ndarray):
@@ -255,14 +256,15 @@ def commit(state: SeqState, out: BlockOut, a: int, t_next: int) -> SeqState:
     return SeqState(kv, state.cross, int(t_next))
 
 
-def verify(model: Model, state: SeqState, drafts) -> VerifyOut:
-    """Score [t0, d_1..d_k] in one pass, accept, emit and commit."""
+def verify(model: Model, state: SeqState, drafts, taps=None) -> VerifyOut:
+    """Score [t0, d_1..d_k] in one pass, accept, emit and commit.  ``taps``: layers whose
+    output residual stream is also returned (no effect on the result)."""
     drafts = [int(t) for t in drafts]
-    out = forward_block(model, state, [state.t0] + drafts)
+    out = forward_block(model, state, [state.t0] + drafts, taps=taps)
     greedy, margins = decide(out.logits)
     a = accept_length(drafts, greedy)
     return VerifyOut(greedy, a, emitted_tokens(greedy, a), margins, out.logits, out.hidden,
-                     commit(state, out, a, greedy[a]), out.new_kv)
+                     commit(state, out, a, greedy[a]), out.new_kv, out.taps)
 
 
 def ar_step(model: Model, state: SeqState) -> VerifyOut:
@@ -330,16 +332,16 @@ def anchor_of(xattn_row: np.ndarray) -> Anchor:
     return Anchor(t, float(mean[t]), top2_margin(mean) if mean.size > 1 else float("inf"), mean)
 
 
-def verify_with_anchor(model: Model, state: SeqState, drafts, layer: int):
+def verify_with_anchor(model: Model, state: SeqState, drafts, layer: int, taps=None):
     """verify() plus the anchor read from the cross-attention at ``layer`` of block row a,
     the last verified position (its output is the bonus token, so its audio attention
     marks where the next draft should start)."""
     drafts = [int(t) for t in drafts]
-    out = forward_block(model, state, [state.t0] + drafts, probe_layer=layer)
+    out = forward_block(model, state, [state.t0] + drafts, probe_layer=layer, taps=taps)
     greedy, margins = decide(out.logits)
     a = accept_length(drafts, greedy)
     res = VerifyOut(greedy, a, emitted_tokens(greedy, a), margins, out.logits, out.hidden,
-                    commit(state, out, a, greedy[a]), out.new_kv)
+                    commit(state, out, a, greedy[a]), out.new_kv, out.taps)
     return res, anchor_of(out.xattn[a])
 
 

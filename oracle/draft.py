@@ -1,12 +1,12 @@
 """Audio-conditioned draft step (test infrastructure only).
 
-Paper, section 3 "Models and Protocol": the draft follows EAGLE-3's direct token
-prediction from multi-layer target features and adds cross-attention from each draft
-step to the frozen audio encoder.  Appendix "Draft architecture": four frozen target
-representations are combined with the current token embedding; one causal block then
-applies self-attention, cross-attention to the frozen audio representation and a
-feed-forward layer, with audio cross-attention at every draft step.  Appendix "Window
-geometry": restricted audio attention uses a +-400 ms half-width around its centre.
+Sources: section 3, paragraph "Models and Protocol" (an EAGLE-3 style drafter that
+predicts tokens directly from features of several target layers, extended so that
+every draft step also attends to the frozen encoder output); appendix "Draft
+architecture" (the drafter's input mixes four target feature vectors with the embedding
+of the current token and feeds a single causal decoder block made of self-attention,
+audio cross-attention and a feed-forward sublayer); appendix "Window geometry" (when the
+audio attention is restricted, it covers 400 ms on each side of its centre).
 
 The paper fixes the shape, not the wiring; the readings used here:
 * The four target representations are the residual stream after target layers L/4,

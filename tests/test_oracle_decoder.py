@@ -166,6 +166,63 @@ def test_spec_loop_with_heads_equals_ar(tiny):
     assert all(0 <= a <= 3 for a in accepts)
 
 
+def test_draft_heads_read_the_last_committed_position(tiny, monkeypatch):
+    """Which hidden row drafts the next block (linear heads on the final hidden state):
+    the LN_f output at the position whose greedy token is the round's bonus token, i.e.
+    the last committed position n' - 1.  Pinned against plain autoregressive decoding
+    (its hidden state at every absolute position) and torch's ``linear`` + ``argmax``:
+    the drafts of every round must be the heads' argmax at AR position n' - 1, and the
+    other block rows must not reproduce them."""
+    cfg, params, enc = tiny
+    model = od.Model(cfg, params)
+    cross = od.cross_kv(model, enc)
+    heads = synth.make_draft_heads(cfg.with_(draft_heads=3))
+    st = od.new_state(model, cross, 1)
+    # AR reference: hidden state of every absolute position 0..N-1
+    N = 30
+    ar_hidden, s = [], st
+    for _ in range(N):
+        r = od.ar_step(model, s)
+        ar_hidden.append(r.hidden[0])
+        s = r.state
+    # record every verify call of the speculative loop: (committed length, drafts, result)
+    calls = []
+    real_verify = od.verify
+
+    def spy(m, state, drafts):
+        out = real_verify(m, state, drafts)
+        calls.append((state.n, [int(t) for t in drafts], out))
+        return out
+
+    monkeypatch.setattr(od, "verify", spy)
+    od.spec_decode_heads(model, st, heads, 24)
+    monkeypatch.undo()
+    W = torch.from_numpy(np.asarray(heads, np.float64))
+
+    def torch_drafts(h, k):
+        hv = torch.from_numpy(np.asarray(h, np.float64))
+        z = [torch.nn.functional.linear(hv, W[i]) for i in range(k)]
+        return [int(torch.argmax(torch.from_numpy(od.round_f32(row.numpy())))) for row in z]
+
+    E = torch.from_numpy(np.asarray(params["tok_emb"], np.float64))
+    other_rows_differ = 0
+    assert len(calls) >= 6
+    for (n_prev, _, prev), (n_cur, drafts, _) in zip(calls, calls[1:]):
+        # the committed length moved by a + 1: the bonus token came from position n_cur - 1
+        assert n_cur == n_prev + prev.accepted + 1
+        h = ar_hidden[n_cur - 1]
+        assert drafts == torch_drafts(h, len(drafts))
+        # that position's LM-head argmax is the round's bonus (pending) token
+        bonus = int(torch.argmax(torch.from_numpy(od.round_f32(
+            torch.nn.functional.linear(torch.from_numpy(h), E).numpy()))))
+        assert bonus == prev.emitted[-1]
+        # any other row of the previous block drafts something else (checked over rounds)
+        for i in range(len(prev.hidden)):
+            if i != prev.accepted and torch_drafts(prev.hidden[i], len(drafts)) != drafts:
+                other_rows_differ += 1
+    assert other_rows_differ >= 3
+
+
 def test_block_clamped_at_last_position(tiny):
     cfg, params, enc = tiny
     model = od.Model(cfg, params)

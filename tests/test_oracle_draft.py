@@ -70,6 +70,35 @@ def test_draft_round_matches_torch_decoder_layer(setup):
     assert r.drafts == [int(np.argmax(od.round_f32(v))) for v in logits]
 
 
+def test_draft_round_recursion(setup):
+    """The step-to-step wiring of a draft round (EAGLE-3 style, section 3 "Models and
+    Protocol"; appendix "Draft architecture"): step 0 reads the fused target feature and
+    the pending token; step j >= 1 reads the block's own output of step j - 1 and the
+    draft it produced.  Every block input is recomputed with torch ``linear`` from the
+    round's recorded outputs; a round that kept the fused feature (or the first token)
+    at every step would give different inputs."""
+    cfg, dcfg, tp, dp, enc, bm, dcross = setup
+    g = np.random.default_rng(3)
+    taps3, hidden = g.standard_normal((3, cfg.d_model)), g.standard_normal(cfg.d_model)
+    token, anchor, K = 29, 40, 5
+    r = odr.draft_round(bm, dp, dcross, taps3, hidden, token, anchor, 90, K)
+    T = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    E = T(tp["tok_emb"])
+    f0 = Fn.linear(T(np.concatenate([taps3.reshape(-1), hidden])), T(dp["w_fuse"]), T(dp["b_fuse"]))
+    feats = [f0] + [T(h) for h in r.hidden[:-1]]
+    toks = [token] + r.drafts[:-1]
+    for j in range(K):
+        u = Fn.linear(torch.cat([feats[j], E[toks[j]]]), T(dp["w_in"]), T(dp["b_in"]))
+        np.testing.assert_allclose(r.inputs[j], u.numpy(), rtol=0, atol=1e-12)
+        if j >= 1:
+            stale = Fn.linear(torch.cat([f0, E[toks[j]]]), T(dp["w_in"]), T(dp["b_in"]))
+            assert np.abs(r.inputs[j] - stale.numpy()).max() > 1e-6
+    # the drafts are the LM-head argmax of each step's output (the tied token table)
+    for j in range(K):
+        z = Fn.linear(T(r.hidden[j]), E).numpy()
+        assert r.drafts[j] == int(np.argmax(od.round_f32(z)))
+
+
 def test_input_projections_match_torch_linear(setup):
     cfg, dcfg, tp, dp, enc, bm, dcross = setup
     g = np.random.default_rng(1)
