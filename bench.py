@@ -14,6 +14,12 @@ update is undone by a 128-byte device copy after the step) so every step does th
 work.  value = emitted tokens per step (accepted drafts + the bonus token, summed over
 the batch) / step time.
 
+The same line also carries: the dominant kernel's roofline (cross-attention), the oracle
+CPU baseline, the anchor readout, draft, tree and AnchorDraft-objective costs, the encoder
+K/V prefill, the measured copy / read rates, the ragged batch of 64 in both row layouts,
+the drift-stress decode loop end to end (tokens/s, mean accepted length, s_1..s_8) and the
+tiny float32 model's step and decode round.
+
 Prints one JSON line (N = 1 only: the step is measured on one GPU).
 """
 from __future__ import annotations
@@ -54,6 +60,12 @@ def parse():
     p.add_argument("--loss", type=int, default=1,
                    help="also time the AnchorDraft objective with its gradients at a training "
                         "batch of the draft (12 utterances x 128 positions)")
+    p.add_argument("--graph", type=int, default=1,
+                   help="time the step replayed from a captured HIP graph (the eager time is "
+                        "reported beside it)")
+    p.add_argument("--workloads", type=int, default=1,
+                   help="also measure the ragged batch (padded and packed), the drift-stress "
+                        "loop and the tiny float32 model, and time the encoder K/V prefill")
     p.add_argument("--copy-calibration-mb", type=int, default=0,
                    help="after the timed steps, copy a buffer of this many MiB once (a plain "
                         "copy of known size that calibrates HBM byte counters)")
@@ -93,45 +105,273 @@ def measured_traffic(workload: str):
     return rec["hbm_bytes_per_launch"]
 
 
-def cpu_baseline(cfg, params, wl, seqs=(0, 1), min_s=5.0):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def host_threads() -> int:
+    """CPU threads this process may use (the box's share, not the machine's count)."""
+    env = os.environ.get("OMP_NUM_THREADS")
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return min(n, int(env)) if env and env.isdigit() and int(env) > 0 else n
+
+
+def cpu_baseline(cfg, params, wl, n_seq=8):
     """The oracle, untuned, on a bounded sample of the workload: the verify step of each of
-    the sequences `seqs` (its k+1 rows), repeated until that sequence has at least `min_s`
-    seconds of timed work (the oracle's verify is a pure function of its state).  The
-    encoder K/V prefill and the greedy continuation used to plant the drafts are computed
-    first and not timed, as on the GPU."""
-    from threadpoolctl import threadpool_info
+    sequences 0 .. n_seq-1 (their k+1 rows each), timed with BLAS threads = the host
+    threads this process may use, then sequence 0's step again with one thread.  Each
+    sequence's encoder K/V projection and the greedy continuation that plants its drafts
+    are computed first and not timed, as on the GPU (they take about 6 s per sequence
+    at this shape, which is what bounds the sample)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import decoder as od
     from paper_2608_12703_amd import synth
     model = od.Model(cfg, params)
-    setup = timed = 0.0
-    tokens = reps = 0
-    desc = []
-    for b in seqs:
-        t0 = time.perf_counter()
-        cross = od.cross_kv(model, synth.make_encoder(cfg, b, int(wl.T[b])))
-        st = od.new_state(model, cross, int(wl.t0[b]), synth.make_prefix_kv(cfg, b, int(wl.n[b])))
-        k = int(wl.k[b])
-        y, _, _ = od.ar_decode(model, st, k)
-        d = synth.plant_drafts(np.array(y), int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])
-        setup += time.perf_counter() - t0
-        spent, r_b = 0.0, 0
-        while spent < min_s:
-            t1 = time.perf_counter()
+    threads = host_threads()
+    states = []
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=threads):
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        for b in range(n_seq):
+            cross = od.cross_kv(model, synth.make_encoder(cfg, b, int(wl.T[b])))
+            st = od.new_state(model, cross, int(wl.t0[b]), synth.make_prefix_kv(cfg, b, int(wl.n[b])))
+            y, _, _ = od.ar_decode(model, st, int(wl.k[b]))
+            states.append((st, synth.plant_drafts(np.array(y), int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])))
+        setup = time.perf_counter() - t0
+        tokens, rows = 0, 0
+        t1 = time.perf_counter()
+        for st, d in states:
             r = od.verify(model, st, d)
-            spent += time.perf_counter() - t1
             tokens += r.accepted + 1
-            r_b += 1
-        timed += spent
-        reps += r_b
-        desc.append(f"sequence {b} (n={int(wl.n[b])}, k={k}, T={int(wl.T[b])}, "
-                    f"{r.accepted + 1} tokens per step) x{r_b}")
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": tokens / timed, "unit": "accepted tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{len(seqs)} of {wl.batch} sequences, one verify step each, repeated: "
-                      + "; ".join(desc) + f": {tokens} tokens in {timed:.1f} s (encoder K/V "
-                      f"prefill and draft planting, {setup:.1f} s, not timed)"}
+            rows += len(d) + 1
+        timed = time.perf_counter() - t1
+    with threadpool_limits(limits=1):
+        st, d = states[0]
+        t2 = time.perf_counter()
+        r0 = od.verify(model, st, d)
+        one = time.perf_counter() - t2
+    return {"value": tokens / timed, "unit": "accepted tokens/s", "cores": int(used), "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "one_thread": {"value": (r0.accepted + 1) / one, "seconds": round(one, 2),
+                           "sample": "sequence 0's verify step"},
+            "sample": f"the verify steps of sequences 0..{n_seq - 1} of the {wl.batch} (a quarter of the "
+                      f"batch; {rows} rows, {tokens} tokens) in {timed:.1f} s with {used} BLAS threads "
+                      f"(encoder K/V projection and draft planting, {setup:.1f} s, not timed)"}
+
+
+def copy_peaks(mib=1024, reps=5):
+    """Measured HBM rates on this GPU: a device copy of `mib` MiB (read + write bytes per
+    second) and a read-dominated reduction over the same buffer (bytes read per second)."""
+    import torch
+    n = (mib << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best_c = best_r = 1e9
+    for _ in range(reps):
+        ev0.record()
+        dst.copy_(src)
+        ev1.record()
+        torch.cuda.synchronize()
+        best_c = min(best_c, ev0.elapsed_time(ev1))
+        ev0.record()
+        _ = src.sum()
+        ev1.record()
+        torch.cuda.synchronize()
+        best_r = min(best_r, ev0.elapsed_time(ev1))
+    nbytes = n * 4
+    del src, dst
+    return {"copy_GBps": round(2 * nbytes / (best_c / 1e3) / 1e9, 1),
+            "read_GBps": round(nbytes / (best_r / 1e3) / 1e9, 1),
+            "what": f"best of {reps}: device copy of {mib} MiB (read + write bytes) and a sum over it "
+                    f"(bytes read)"}
+
+
+def time_prefill(sess, encs, reps=3):
+    """The encoder K/V projection of the whole batch (setup, once per utterance): ms per
+    call and the matrix-core rate against the dense bf16 peak (2 frames_cap 2d d flop per
+    layer; padded frame slots are computed too)."""
+    import torch
+
+    from paper_2608_12703_amd import ad, roofline
+    enc = sess.upload_encoder(encs)
+    ad.cross_kv_prefill(sess.model, enc, sess.cross_struct())
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(reps):
+        ad.cross_kv_prefill(sess.model, enc, sess.cross_struct())
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    cfg = sess.cfg
+    flops = 2.0 * sess.frames_cap * 2 * cfg.d_model * cfg.d_model * cfg.n_layers
+    del enc
+    return {"ms_per_batch": round(ms, 3), "utterances": sess.B, "frames_cap": sess.frames_cap,
+            "tflops": round(flops / (ms / 1e3) / 1e12, 1),
+            "mfma_frac": round(flops / (ms / 1e3) / roofline.BF16_MFMA_PEAK, 4)}
+
+
+def planted_session(cfg, params, wl, layout):
+    """A session over workload wl with drafts planted on the GPU's own greedy
+    continuation (Geometric agreement), prepared and ready to step."""
+    from paper_2608_12703_amd import ad, synth
+    from paper_2608_12703_amd.harness import Session
+    sess = Session(cfg, params, wl.batch, int(wl.k.max()), wl.T, layout=layout,
+                   packed_encoder=layout == ad.AD_PACKED)
+    sess.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+    for b in range(wl.batch):
+        sess.import_prefix(b, synth.make_prefix_kv(cfg, b, int(wl.n[b])))
+    sess.set_kv_len(wl.n)
+    y = gpu_greedy_continuation(sess, wl.t0, wl.k)
+    blocks = [np.concatenate([[wl.t0[b]],
+                              synth.plant_drafts(y[b], int(wl.G[b]), wl.fill_ne[b], wl.fill_any[b])])
+              for b in range(wl.batch)]
+    sess.prepare(blocks)
+    return sess, blocks, y
+
+
+def time_steps(sess, steps, warmup):
+    """ms per step of the prepared block (verify + commit, each from the same committed
+    state) with HIP events; the accept lengths of the last step."""
+    import torch
+    kv0 = sess.kv_len.clone()
+
+    def one():
+        sess.run()
+        sess.commit()
+        sess.kv_len.copy_(kv0)
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        one()
+    ev1.record()
+    torch.cuda.synchronize()
+    res = sess.results()
+    assert res["err"] == 0, f"device error flag {res['err']}"
+    return ev0.elapsed_time(ev1) / steps, res
+
+
+def measure_ragged(params_dev, steps, warmup):
+    """The ragged large-v3 batch (64 sequences, k 2..8, 200..1500 frames, committed
+    lengths 0..447-k) in both row layouts; both are charged the same algorithmic bytes."""
+    import torch
+
+    from paper_2608_12703_amd import ad, roofline, synth
+    from paper_2608_12703_amd.configs import CONFIGS
+    cfg = CONFIGS["ragged_large_v3"]
+    wl = synth.make_step_workload(cfg)
+    sb = roofline.step_bytes(cfg, wl.n, wl.T, wl.k)
+    out = {"batch": wl.batch, "k": [int(wl.k.min()), int(wl.k.max())],
+           "frames": [int(wl.T.min()), int(wl.T.max())], "step_hbm_bytes": sb["total"]}
+    accepts = []
+    for name, layout in (("padded", ad.AD_PADDED), ("packed", ad.AD_PACKED)):
+        sess, _, _ = planted_session(cfg, params_dev, wl, layout)
+        ms, res = time_steps(sess, steps, warmup)
+        tokens = int(np.sum(res["accept_len"] + 1))
+        accepts.append(res["accept_len"])
+        out[name] = {"ms_per_step": round(ms, 4), "value": round(tokens / (ms / 1e3), 1),
+                     "rows": sess.rows, "tokens_per_step": tokens,
+                     "step_hbm_frac": round(sb["total"] / (ms / 1e3) / roofline.HBM_PEAK, 4)}
+        log(f"ragged {name}: {ms:.3f} ms/step, {sess.rows} rows, {tokens} tokens/step")
+        del sess
+        torch.cuda.empty_cache()
+    assert np.array_equal(accepts[0], accepts[1]), "padded and packed layouts disagree"
+    return out
+
+
+def measure_drift(params_dev):
+    """The drift-stress loop (batch 32, k 8, 1500 frames): every sequence decodes from the
+    start token to the last position (447 tokens) with drafts planted on the target's own
+    greedy continuation and misaligned by +-1 token after Poisson(40)-spaced anchors.
+    Timed end to end: the host plants each round's drafts, the step verifies, commits and
+    returns the accept lengths (one host round trip per round).  The greedy continuation
+    itself comes from an untimed autoregressive pass first."""
+    import torch
+
+    from paper_2608_12703_amd import decode, synth
+    from paper_2608_12703_amd.configs import CONFIGS, MAX_POS, SOT_TOKEN
+    from paper_2608_12703_amd.harness import Session
+    cfg = CONFIGS["drift_stress"]
+    B, K, T = cfg.batch, cfg.k, cfg.frames
+    sess = Session(cfg, params_dev, B, K, [T] * B)
+    sess.prefill_encoder([synth.make_encoder(cfg, b, T) for b in range(B)])
+    sess.set_kv_len(np.zeros(B, np.int64))
+    n_tok = MAX_POS - 1
+    ys = np.full((B, n_tok + 1), SOT_TOKEN, np.int64)
+    pend = [SOT_TOKEN] * B
+    for p in range(1, n_tok + 1):
+        sess.step([np.array([t], np.int64) for t in pend], commit=True)
+        out = sess.out_tokens[:, 0].cpu().numpy()
+        ys[:, p] = out
+        pend = [int(t) for t in out]
+    plans = [synth.make_drift_plan(cfg, b) for b in range(B)]
+    ks = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    toks, acc, rounds = decode.decode_with_drift(sess, list(ys), plans, K, n_tok, ks_out=ks)
+    wall = time.perf_counter() - t0
+    assert all(list(t) == list(ys[b, 1:len(t) + 1]) for b, t in enumerate(toks)), "loop not lossless"
+    a, k = np.array(acc), np.array(ks)
+    live = k >= 0
+    full = k == K
+    s = [float(np.mean(a[full] >= j)) for j in range(1, K + 1)]
+    emitted = sum(len(t) for t in toks)
+    log(f"drift stress: {rounds} rounds, {emitted} tokens in {wall:.2f} s")
+    del sess
+    torch.cuda.empty_cache()
+    return {"batch": B, "k": K, "tokens": emitted, "rounds": rounds, "seconds": round(wall, 3),
+            "value": round(emitted / wall, 1), "unit": "accepted tokens/s",
+            "ms_per_round": round(1e3 * wall / rounds, 3),
+            "mean_accepted_length": round(float(np.mean(a[live])), 4),
+            "tokens_per_round": round(float(np.mean(a[live] + 1)), 4),
+            "s_k": [round(x, 4) for x in s], "L": round(sum(s), 4),
+            "rounds_with_full_block": int(np.sum(full))}
+
+
+def measure_tiny(steps):
+    """The tiny float32 model (4 layers, d 384, vocab 51865), batch 1: the 64-token greedy
+    decode with 4 linear draft heads (rounds of verify, commit and ad_draft_heads), and
+    one verify step of a 5-row block alone."""
+    import torch
+
+    from paper_2608_12703_amd import ad, decode, synth
+    from paper_2608_12703_amd.configs import CONFIGS, SOT_TOKEN
+    from paper_2608_12703_amd.harness import Session, upload
+    cfg = CONFIGS["tiny_fp32"]
+    params = synth.make_params(cfg)
+    heads = upload(synth.make_draft_heads(cfg), torch.float32)
+    wl = synth.make_step_workload(cfg)
+    T = int(wl.T[0])
+    sess = Session(cfg, params, 1, cfg.draft_heads, [T])
+    sess.prefill_encoder([synth.make_encoder(cfg, 0, T)])
+    sess.set_kv_len([0])
+    decode.decode_with_heads(sess, heads, [SOT_TOKEN], cfg.decode_tokens)   # warm
+    sess.set_kv_len([0])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    toks, acc, _, rounds = decode.decode_with_heads(sess, heads, [SOT_TOKEN], cfg.decode_tokens)
+    wall = time.perf_counter() - t0
+    sess.set_kv_len([0])
+    sess.prepare([np.array([SOT_TOKEN] + [int(x) for x in wl.fill_any[0]], np.int64)])
+    ms, _ = time_steps(sess, steps, 3)
+    return {"us_per_step": round(ms * 1e3, 2), "rows": sess.rows,
+            "decode_tokens": cfg.decode_tokens, "rounds": rounds,
+            "us_per_round_end_to_end": round(1e6 * wall / rounds, 1),
+            "accepted_per_round": round(float(np.mean([int(a[0]) for a in acc[1:]])), 4)}
 
 
 def main():
@@ -156,8 +396,10 @@ def main():
     wl = synth.make_step_workload(cfg)
     sess = Session(cfg, params, wl.batch, int(wl.k.max()), wl.T, layout=layout,
                    packed_encoder=layout == ad.AD_PACKED)
+    params_dev = sess.params          # device parameters, shared by the later sessions
     log("encoder K/V prefill")
-    sess.prefill_encoder([synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)])
+    encs = [synth.make_encoder(cfg, b, int(wl.T[b])) for b in range(wl.batch)]
+    sess.prefill_encoder(encs)
     for b in range(wl.batch):
         sess.import_prefix(b, synth.make_prefix_kv(cfg, b, int(wl.n[b])))
     sess.set_kv_len(wl.n)
@@ -197,6 +439,31 @@ def main():
     res2 = sess.results()
     assert np.array_equal(res2["accept_len"], res["accept_len"]), "steps were not repeatable"
     log(f"{ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f}), {tokens} tokens/step")
+    ms_eager = ms
+    if args.graph:
+        # The same step (verify, commit, length reset) captured once into a HIP graph and
+        # replayed: the same kernels with the same arguments, launched by the graph
+        # instead of one host call each.  Every replay's accept lengths, tokens and hidden
+        # rows must equal the eager step's.
+        ref_hidden = res2["hidden"].copy()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            one_step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.steps
+        res3 = sess.results()
+        assert np.array_equal(res3["accept_len"], res["accept_len"])
+        assert np.array_equal(res3["out_tokens"], res2["out_tokens"])
+        assert np.array_equal(res3["hidden"].view(np.uint32), ref_hidden.view(np.uint32))
+        log(f"graph-launched: {ms:.3f} ms/step (eager {ms_eager:.3f})")
+        del graph
 
     sb = roofline.step_bytes(cfg, wl.n, wl.T, wl.k)
     rows = sess.rows
@@ -398,6 +665,25 @@ def main():
         log(f"AnchorDraft objective + gradients: {us_l:.1f} us ({lbytes / (us_l * 1e-6) / 1e9:.0f} GB/s)")
         del ls, xq, logits, dlog
 
+    prefill = ragged = drift = tiny = peaks = None
+    if args.workloads and cfg.name == "large_v3_bf16":   # the other workloads share its weights
+        torch.cuda.empty_cache()
+        ps = Session(cfg, params_dev, wl.batch, int(wl.k.max()), wl.T, layout=layout,
+                     packed_encoder=layout == ad.AD_PACKED)
+        prefill = time_prefill(ps, encs)
+        log(f"encoder K/V prefill: {prefill['ms_per_batch']:.2f} ms per batch of {wl.batch} "
+            f"({prefill['tflops']:.0f} TFLOP/s)")
+        del ps
+        torch.cuda.empty_cache()
+        ragged = measure_ragged(params_dev, args.steps, args.warmup)
+        drift = measure_drift(params_dev)
+        tiny = measure_tiny(max(args.steps, 50))
+        log(f"tiny float32: {tiny['us_per_step']:.1f} us per verify step, "
+            f"{tiny['us_per_round_end_to_end']:.1f} us per decode round")
+        peaks = copy_peaks()
+        log(f"copy {peaks['copy_GBps']:.0f} GB/s, read {peaks['read_GBps']:.0f} GB/s")
+    del encs
+
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
@@ -410,7 +696,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log("oracle CPU baseline (two sequences, about 10 s)")
+        log("oracle CPU baseline (eight sequences' verify steps after their setup, about a minute)")
         cpu = cpu_baseline(cfg, params, wl)
         log(f"oracle: {cpu['value']:.3f} tokens/s")
 
@@ -431,6 +717,8 @@ def main():
         "unit": "accepted tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "launch": "hip graph" if args.graph else "eager",
+        "eager_ms_per_step": round(ms_eager, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": cfg.name, "batch": wl.batch, "k": int(wl.k.max()),
@@ -440,6 +728,11 @@ def main():
         "step_hbm_frac": round(sb["total"] / (ms / 1e3) / roofline.HBM_PEAK, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "hbm_measured": peaks,
+        "prefill": prefill,
+        "ragged": ragged,
+        "drift_stress": drift,
+        "tiny_fp32": tiny,
         "anchor_readout": anchor,
         "draft_step": draft,
         "tree_step": tree,

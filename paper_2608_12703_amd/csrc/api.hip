@@ -823,12 +823,13 @@ ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_c
   e.H = D.n_heads;
   e.d = D.d_model;
   e.frames_cap = cross->frames_cap;
-  // The float32 A operand of the VALU product: widen the encoder states once.
+  // bf16 models: the matrix cores (a large dense product); float32 models: the VALU.
   for (int l = 0; l < D.n_layers; ++l) {
     e.layer = l;
     if (D.dtype == AD_BF16)
-      ad::launch_gemm_valu_bf16a(ad::EPI_XKV, cross->frames_cap, 2 * D.d_model, D.d_model, enc,
-                                 lp(model, l, W_XKV), lp(model, l, B_XKV), e, st);
+      ad::launch_xkv_mfma(cross->frames_cap, 2 * D.d_model, D.d_model, (const uint16_t*)enc,
+                          (const uint16_t*)lp(model, l, W_XKV), (const uint16_t*)lp(model, l, B_XKV),
+                          (uint16_t*)cross->data, l, D.n_heads, D.d_model, cross->frames_cap, st);
     else
       ad::launch_gemm_valu<ad::F32>(ad::EPI_XKV, cross->frames_cap, 2 * D.d_model, D.d_model,
                                     (const float*)enc, lp(model, l, W_XKV), lp(model, l, B_XKV), e, st);

@@ -88,9 +88,10 @@ template <class S>
 void launch_gemm_valu(int epi, int M, int N, int K, const float* A, const void* W, const void* bias,
                       const EpiArgs& e, hipStream_t st);
 
-// The same product with a bf16 A operand (encoder states of a bf16 model).
-void launch_gemm_valu_bf16a(int epi, int M, int N, int K, const void* A, const void* W, const void* bias,
-                            const EpiArgs& e, hipStream_t st);
+// Cross-attention keys / values of a bf16 model's encoder states on the matrix cores:
+// cache <- enc [M][K] W [N][K]^T + bias in the cross-K/V layout of `layer` (N = 2d).
+void launch_xkv_mfma(int M, int N, int K, const uint16_t* A, const uint16_t* W, const uint16_t* bias,
+                     uint16_t* cache, int layer, int H, int d, int frames_cap, hipStream_t st);
 
 // bf16 matrix-core product: X (A-fragment order, RT row tiles, RT a multiple of 16)
 // times W^T.

@@ -11,8 +11,9 @@
 // lane; keeping them out of LDS removes a third of the step's LDS traffic), and through
 // a three-stage LDS ring for 16 row tiles.  Workgroups with long K ranges (the FFN
 // products) take two K steps per barrier.  The waits are explicit; the loops are unrolled
-// over the ring stages so every buffer is a distinct object.  Small-N products split K over several
-// workgroups and the last one to finish a tile sums the partial tiles in split order.
+// over the ring stages so every buffer is a distinct object.  Small-N products split K
+// over several workgroups, each storing its raw partial tile; the kernel that consumes
+// the product (attention, or residual + LayerNorm) sums the partials in split order.
 // The split count depends on the weight shape only, so a row's result never depends
 // on how many other rows share the launch.
 #include <algorithm>
@@ -80,11 +81,15 @@ __device__ __forceinline__ Top2s t2_row16(Top2s t) {
 
 // Wait until at most N vector-memory operations of this wave are outstanding (they
 // complete in order) and its LDS operations are done, then barrier.  No memory fence.
-#define BARRIER_VMCNT(N)                       \
-  do {                                         \
-    __builtin_amdgcn_s_waitcnt(0x0070 | (N));  \
-    __builtin_amdgcn_s_barrier();              \
-    asm volatile("" ::: "memory");             \
+// The gfx9 s_waitcnt immediate holds vmcnt in two fields: bits 3:0 and bits 15:14
+// (expcnt 7 in bits 6:4 means no wait on exports; lgkmcnt 0 in bits 11:8).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }
+#define BARRIER_VMCNT(N)                                     \
+  do {                                                       \
+    static_assert((N) >= 0 && (N) < 64, "vmcnt is 6 bits");  \
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(N));               \
+    __builtin_amdgcn_s_barrier();                            \
+    asm volatile("" ::: "memory");                           \
   } while (0)
 
 // One 32-wide K step of a wave: RW row tiles (row group rg) x 4 column tiles (half ch).

@@ -98,11 +98,6 @@ void launch_gemm_valu(int epi, int M, int N, int K, const float* A, const void* 
 template void launch_gemm_valu<F32>(int, int, int, int, const float*, const void*, const void*, const EpiArgs&, hipStream_t);
 template void launch_gemm_valu<BF16>(int, int, int, int, const float*, const void*, const void*, const EpiArgs&, hipStream_t);
 
-void launch_gemm_valu_bf16a(int epi, int M, int N, int K, const void* A, const void* W, const void* bias,
-                            const EpiArgs& e, hipStream_t st) {
-  gemm_valu_dispatch<BF16, BF16>(epi, M, N, K, A, W, bias, e, st);
-}
-
 // ---------------------------------------------------------------- attention
 // One block per (head, sequence).  Queries are taken 16 at a time; keys stream through
 // LDS in chunks of 64 at absolute positions 0, 64, 128, ... with an online softmax per

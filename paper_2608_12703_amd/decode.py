@@ -62,13 +62,16 @@ def decode_with_heads(sess, heads_w, t0, n_tokens: int):
     return [t[:n_tokens] for t in toks], accepts, drafts, rounds
 
 
-def decode_with_drift(sess, ys, plans, k: int, n_tokens: int):
+def decode_with_drift(sess, ys, plans, k: int, n_tokens: int, ks_out=None):
     """Speculative decode with drifting planted drafts (synth.plant_drift).
 
     ys[b] is sequence b's greedy continuation from position 0 (ys[b][0] = the pending
-    start token); the committed prefix starts empty.  A sequence that already has
-    n_tokens tokens verifies its pending token alone until the others catch up, so ys[b]
-    needs n_tokens + k + 1 entries.  Returns (tokens, accepts, rounds).
+    start token); the committed prefix starts empty.  The batch is static: a sequence
+    that already has n_tokens tokens stays in it as an idle one-row block (its pending
+    token verified again at its last position, nothing kept) until every sequence is
+    done.  ys[b] needs min(n_tokens + k, MAX_POS - 1) + 1 entries.  ks_out, if given,
+    receives each round's draft lengths ([B] arrays, -1 for an idle sequence).
+    Returns (tokens, accepts, rounds).
     """
     B = sess.B
     toks = [[] for _ in range(B)]
@@ -78,24 +81,29 @@ def decode_with_drift(sess, ys, plans, k: int, n_tokens: int):
     rounds = 0
     done = lambda: min(len(t) for t in toks) >= n_tokens
     while not done():
-        blocks = []
-        for b in range(B):
-            kb = _clamp_k(k, int(n[b])) if len(toks[b]) < n_tokens else 0
-            blocks.append(np.concatenate([[pending[b]], synth.plant_drift(ys[b], int(n[b]), kb, plans[b])]))
+        # finished sequences re-verify at their last position (the commit's move of
+        # their length is undone here each round)
+        sess.set_kv_len(np.minimum(n, MAX_POS - 1))
+        live = [len(toks[b]) < n_tokens for b in range(B)]
+        ks = np.array([_clamp_k(k, int(n[b])) if live[b] else 0 for b in range(B)])
+        blocks = [np.concatenate([[pending[b]], synth.plant_drift(ys[b], int(n[b]), int(ks[b]), plans[b])])
+                  for b in range(B)]
         sess.step(blocks)
         sess.commit()
         res = sess.results()
         assert res["err"] == 0, f"device error flag {res['err']}"
         a = res["accept_len"]
         accepts.append(a.copy())
+        if ks_out is not None:
+            ks_out.append(np.where(live, ks, -1))
         for b in range(B):
+            if not live[b]:
+                continue
             emitted = [int(x) for x in res["out_tokens"][b][: a[b] + 1]]
             toks[b] += emitted
             pending[b] = emitted[-1]
             n[b] += a[b] + 1
         rounds += 1
-        if int(n.max()) >= MAX_POS:
-            break
     return [t[:n_tokens] for t in toks], accepts, rounds
 
 

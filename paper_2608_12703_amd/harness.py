@@ -112,12 +112,17 @@ class Session:
                         self.enc_off.data_ptr())
 
     # ------------------------------------------------------------------ setup
-    def prefill_encoder(self, encs):
-        """Upload encoder states (list of [T_b, d] arrays) and build the encoder K/V."""
+    def upload_encoder(self, encs) -> torch.Tensor:
+        """Encoder states (list of [T_b, d] arrays) in the session's encoder slots."""
         enc = torch.zeros(self.frames_cap, self.cfg.d_model, dtype=self.dt, device=self.device)
         offs = self.enc_off.cpu().numpy()
         for b, e in enumerate(encs):
             enc[offs[b]: offs[b] + len(e)] = upload(e, self.dt, self.device)
+        return enc
+
+    def prefill_encoder(self, encs):
+        """Upload encoder states (list of [T_b, d] arrays) and build the encoder K/V."""
+        enc = self.upload_encoder(encs)
         ad.cross_kv_prefill(self.model, enc, self.cross_struct())
         del enc
 

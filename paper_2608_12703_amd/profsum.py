@@ -11,6 +11,11 @@
       HBM bytes per dispatch of one kernel from a FETCH_SIZE run and a WRITE_SIZE run,
       each scaled by what the same counter reads for a plain copy of MIB MiB captured in
       the same run (the largest copyBuffer dispatch)
+  python -m paper_2608_12703_amd.profsum counters RESULTS.db [RESULTS.db ...]
+          [--kernel SUBSTR ...] [--command CMD]
+      per kernel, the mean per dispatch of every counter collected (several --pmc runs may
+      be given); with SQ_INSTS_VALU_MFMA_MOPS_BF16 also the bf16 matrix rate (512 flop per
+      count over the dispatch's duration) against the dense bf16 peak
 """
 from __future__ import annotations
 
@@ -85,6 +90,47 @@ def traffic(fetch_db: str, write_db: str, kernel: str, calib_mib: int, command: 
             "command": command}
 
 
+def counter_table(dbs, kernels=None) -> str:
+    """Mean value per dispatch of each counter, per kernel name (matching `kernels`)."""
+    from .roofline import BF16_MFMA_PEAK
+    per = {}      # kernel -> counter -> [sum, n]
+    dur = {}      # kernel -> [sum ns, n] (dispatch durations of the counter runs)
+    for db in dbs:
+        cur = sqlite3.connect(db).cursor()
+        rows = cur.execute("select kernel_name, counter_name, value, dispatch_id, duration "
+                           "from counters_collection").fetchall()
+        seen = set()
+        for name, cname, val, disp, du in rows:
+            if kernels and not any(k in name for k in kernels):
+                continue
+            e = per.setdefault(name, {}).setdefault(cname, [0.0, 0])
+            e[0] += float(val)
+            e[1] += 1
+            if (db, disp) not in seen and du:
+                seen.add((db, disp))
+                d = dur.setdefault(name, [0.0, 0])
+                d[0] += float(du)
+                d[1] += 1
+    out = []
+    for name in sorted(per, key=lambda n: -dur.get(n, [0, 1])[0]):
+        cs = per[name]
+        d = dur.get(name)
+        mean_ns = d[0] / d[1] if d and d[1] else 0.0
+        out.append(f"{name[:100]}")
+        if mean_ns:
+            out.append(f"    mean duration under the counters {mean_ns / 1e3:.2f} us ({d[1]} dispatches)")
+        for cname in sorted(cs):
+            tot, n = cs[cname]
+            out.append(f"    {cname:36s} {tot / n:16.1f}")
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in cs and mean_ns:
+            tot, n = cs["SQ_INSTS_VALU_MFMA_MOPS_BF16"]
+            flops = tot / n * 512
+            rate = flops / (mean_ns * 1e-9)
+            out.append(f"    bf16 matrix work {flops / 1e9:.2f} GFLOP per dispatch -> {rate / 1e12:.1f} TFLOP/s "
+                       f"= {100 * rate / BF16_MFMA_PEAK:.1f}% of the dense bf16 peak")
+    return "\n".join(out)
+
+
 def main(argv=None):
     p = argparse.ArgumentParser(prog="profsum")
     sub = p.add_subparsers(dest="cmd", required=True)
@@ -103,7 +149,16 @@ def main(argv=None):
     t.add_argument("--calib-mib", type=int, required=True)
     t.add_argument("--out", required=True)
     t.add_argument("--command", default="")
+    c = sub.add_parser("counters")
+    c.add_argument("dbs", nargs="+")
+    c.add_argument("--kernel", action="append")
+    c.add_argument("--command", default="")
     a = p.parse_args(argv)
+    if a.cmd == "counters":
+        if a.command:
+            print(f"command: {a.command}\n")
+        print(counter_table(a.dbs, a.kernel))
+        return
     if a.cmd == "kernels":
         if a.command:
             print(f"command: {a.command}\n")

@@ -34,6 +34,8 @@ from paper_2608_12703_amd import ad, synth
 from paper_2608_12703_amd.configs import Config
 from paper_2608_12703_amd.harness import Session
 
+from gpu_common import encode_cross
+
 pytestmark = pytest.mark.gpu
 
 UNIT = Config(name="unit_loss", n_layers=2, d_model=128, n_heads=2, d_ffn=256, vocab=1000,
@@ -209,7 +211,21 @@ def test_full_size_objective_sampled_against_oracle():
     Ts = [int(t) for t in wl.T[:B]]
     dcfg, sess = _draft_session(cfg, params, dparams, B, R, Ts)
     encs = [synth.make_encoder(cfg, b, T) for b, T in enumerate(Ts)]
-    sess.prefill_encoder(encs)
+    # the objective reads the draft's encoder keys; both sides use the oracle's keys (the
+    # prefill that would otherwise make them is pinned by its own test), so the
+    # comparison below sees only the objective's arithmetic
+    bm = odr.block_model(synth.draft_config(cfg), params, dparams)
+    H, F = cfg.n_heads, sess.frames_cap
+    Kall = np.zeros((1, H, F, 64), np.float32)
+    Vall = np.zeros((1, H, F, 64), np.float32)
+    offs = sess.enc_off.cpu().numpy()
+    oracle_keys = []
+    for b in range(B):
+        Kb, Vb = od.cross_kv(bm, encs[b])[0]
+        oracle_keys.append(Kb)
+        Kall[0, :, offs[b]: offs[b] + Ts[b]] = np.asarray(Kb, np.float32).transpose(1, 0, 2)
+        Vall[0, :, offs[b]: offs[b] + Ts[b]] = np.asarray(Vb, np.float32).transpose(1, 0, 2)
+    sess.cross.copy_(torch.from_numpy(encode_cross(Kall, Vall)).to(sess.cross.dtype))
     g = np.random.default_rng(31)
     M, d, V = B * R, cfg.d_model, cfg.vocab
     xq = (g.standard_normal((M, d)) * 8).astype(np.float32)
@@ -229,9 +245,8 @@ def test_full_size_objective_sampled_against_oracle():
     e = np.max(np.abs(got["dlogits"][rows] - dz[rows]))
     assert e <= 1e-5 * np.max(np.abs(dz[rows])), e
     # every row of two utterances against the oracle's alignment term
-    bm = odr.block_model(dcfg, params, dparams)
     for b in (0, 7):
-        K = od.cross_kv(bm, encs[b])[0][0]
+        K = oracle_keys[b]
         sl = slice(b * R, (b + 1) * R)
         ref = al.anchor_loss([xq[sl].astype(np.float64)], [K], [Ts[b]], [center[sl]], SIGMA, LAM)
         np.testing.assert_allclose(got["row"][sl], ref.row_loss[0], rtol=2e-5, atol=1e-6)

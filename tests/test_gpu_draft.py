@@ -177,4 +177,6 @@ def test_large_v3_draft_round_sampled():
     print(f"  seq {b_s}: a={a} anchor={anc.frame} drafts gpu {got[b_s].tolist()} oracle {want.drafts} "
           f"(compared {cut}), margins {np.round(want.margins, 4).tolist()}")
     assert got[b_s][:cut].tolist() == want.drafts[:cut]
-    assert cut >= 1
+    # this sequence's oracle draft margins are all >= 1e-3 (smallest 0.0043, at step 5),
+    # so every draft is compared; fewer than three would mean the oracle changed
+    assert cut >= 3, f"only {cut} drafts comparable (oracle margins {want.margins})"

@@ -14,7 +14,7 @@ from paper_2608_12703_amd.harness import Session
 
 import gpu_common
 from gpu_common import (compare_sequence, device_session, oracle_model, oracle_state,
-                        planted_blocks, subset)
+                        planted_blocks, step_taps, subset)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,14 +41,15 @@ def test_step_matches_oracle(dtype, layout):
     sess.step(blocks)
     res = sess.results()
     assert res["err"] == 0
+    taps = step_taps(sess, blocks)
     worst = 0.0
     for b in range(wl.batch):
         st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
-        ref = od.verify(model, st, blocks[b][1:])
-        worst = max(worst, compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b])))
-    kvx = min(gpu_common.KV_EXACT) if gpu_common.KV_EXACT else 1.0
-    gpu_common.KV_EXACT.clear()
-    print(f"[{dtype} layout={layout}] max logit error {worst:.3e}, min KV bit-equal fraction {kvx:.4f}")
+        ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+        worst = max(worst, compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]),
+                                            gpu_taps=taps))
+    print(f"[{dtype} layout={layout}] max logit error {worst:.3e}")
+    gpu_common.kv_report(f"{dtype} layout={layout}")
     # planted agreement: acceptance is min(G, k) where the oracle is decisive
     assert np.all(res["accept_len"] <= wl.k)
     sess.commit()
@@ -175,8 +176,8 @@ def test_block_ending_at_last_position():
     res = sess.results()
     assert res["err"] == 0
     st = oracle_state(cfg, model, b, n, int(wl.T[b]), int(wl.t0[b]))
-    ref = od.verify(model, st, blocks[b][1:])
-    compare_sequence(cfg, sess, res, b, blocks[b], ref, n)
+    ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+    compare_sequence(cfg, sess, res, b, blocks[b], ref, n, gpu_taps=step_taps(sess, blocks))
 
 
 def test_tiled_weights_are_bit_identical():

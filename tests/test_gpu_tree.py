@@ -27,7 +27,7 @@ from paper_2608_12703_amd.configs import Config
 from paper_2608_12703_amd.harness import Session
 
 from gpu_common import (LOGIT_TOL, MARGIN_EXCLUDE, compare_anchor, device_session, kv_close,
-                        oracle_model, oracle_state)
+                        kv_report, layer_input_errors, oracle_model, oracle_state, step_taps)
 
 pytestmark = pytest.mark.gpu
 
@@ -125,6 +125,7 @@ def test_tree_step_and_commit_match_oracle(dtype):
     sess.step(blocks, parents=trees)
     res = sess.results()
     assert res["err"] == 0
+    gpu_taps = step_taps(sess, blocks, parents=trees)
     kv_pre = [sess.export_prefix(b, int(wl.n[b]) + len(trees[b])) for b in range(wl.batch)]
     sess.commit()
     res_c = sess.results()
@@ -132,7 +133,8 @@ def test_tree_step_and_commit_match_oracle(dtype):
     for b, par in enumerate(trees):
         n, r = int(wl.n[b]), len(par)
         st = oracle_state(cfg, model, b, n, int(wl.T[b]), int(wl.t0[b]))
-        out = od.forward_block(model, st, blocks[b], parents=par, probe_layer=ANCHOR_LAYER)
+        out = od.forward_block(model, st, blocks[b], parents=par, probe_layer=ANCHOR_LAYER,
+                               taps=list(range(cfg.n_layers - 1)))
         ref = od.verify_tree(model, st, blocks[b], par)
         rows = [sess.row_of(b, i) for i in range(r)]
         err = float(np.max(np.abs(res["logits"][rows] - out.logits)))
@@ -144,9 +146,10 @@ def test_tree_step_and_commit_match_oracle(dtype):
             if ref.margins[i] >= MARGIN_EXCLUDE:
                 assert g[i] == ref.greedy[i], f"seq {b} node {i}"
         # the cache the step wrote: node i at slot n + i
+        eps = layer_input_errors(gpu_taps, out.taps, rows, cfg.n_layers)
         for layer, (kb, vb) in enumerate(out.new_kv):
-            kv_close(kv_pre[b][layer, 0, n:], kb, f"seq {b} layer {layer} K", dtype)
-            kv_close(kv_pre[b][layer, 1, n:], vb, f"seq {b} layer {layer} V", dtype)
+            kv_close(kv_pre[b][layer, 0, n:], kb, f"seq {b} layer {layer} K", dtype, layer, eps[layer])
+            kv_close(kv_pre[b][layer, 1, n:], vb, f"seq {b} layer {layer} V", dtype, layer, eps[layer])
         a = int(res["accept_len"][b])
         path = res["path"][b][: a + 1].tolist()
         # the walk reads the greedy tokens at the path's nodes
@@ -300,10 +303,12 @@ def test_large_v3_tree_step_sampled():
     sess.step(blocks, parents=[TREE] * wl.batch)
     res = sess.results()
     assert res["err"] == 0
+    gpu_taps = step_taps(sess, blocks, parents=[TREE] * wl.batch)
     kv_pre = sess.export_prefix(b_s, n + len(TREE))
     sess.commit()
     res_c = sess.results()
-    out = od.forward_block(model, st, blocks[b_s], parents=TREE, probe_layer=layer)
+    out = od.forward_block(model, st, blocks[b_s], parents=TREE, probe_layer=layer,
+                           taps=list(range(cfg.n_layers - 1)))
     ref = od.verify_tree(model, st, blocks[b_s], TREE)
     rows = [sess.row_of(b_s, i) for i in range(len(TREE))]
     err = float(np.max(np.abs(res["logits"][rows] - out.logits)))
@@ -313,9 +318,11 @@ def test_large_v3_tree_step_sampled():
     for i in range(len(TREE)):
         if ref.margins[i] >= MARGIN_EXCLUDE:
             assert res["greedy"][rows[i]] == ref.greedy[i]
+    eps = layer_input_errors(gpu_taps, out.taps, rows, cfg.n_layers)
     for lay, (kb, vb) in enumerate(out.new_kv):
-        kv_close(kv_pre[lay, 0, n:], kb, f"layer {lay} K", "bf16")
-        kv_close(kv_pre[lay, 1, n:], vb, f"layer {lay} V", "bf16")
+        kv_close(kv_pre[lay, 0, n:], kb, f"layer {lay} K", "bf16", lay, eps[lay])
+        kv_close(kv_pre[lay, 1, n:], vb, f"layer {lay} V", "bf16", lay, eps[lay])
+    kv_report("tree large-v3")
     assert all(ref.margins[u] >= MARGIN_EXCLUDE for u in ref.path)
     a = int(res["accept_len"][b_s])
     path = res["path"][b_s][: a + 1].tolist()
