@@ -249,6 +249,22 @@ ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_c
 ad_status ad_verify_step(const ad_model* model, const ad_step* step, void* stream);
 
 /*
+ * ad_verify_step without a caller workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  step->workspace and step->workspace_bytes are ignored; the step runs in
+ * a library-owned static device buffer of 64 MiB (AD_STATIC_SCRATCH_BYTES) that every
+ * GPU the library runs on holds until the process ends.  Nothing is allocated or freed
+ * by the call.  The results are those of ad_verify_step with a workspace (same kernels).
+ * Every call on one GPU shares that GPU's buffer: calls that overlap on one GPU (on
+ * different streams, or from different threads) race and give undefined results.  The
+ * large-v3 bench step (224 rows, 32 sequences, k_max 6) needs 45.7 MiB.
+ * Errors: as ad_verify_step; AD_ENOSPACE when ad_workspace_size() of the step exceeds
+ * AD_STATIC_SCRATCH_BYTES; AD_EHIP if the buffer's device address cannot be obtained.
+ */
+#define AD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+ad_status ad_verify_step_static(const ad_model* model, const ad_step* step, void* stream);
+
+/*
  * Input rows of the audio-conditioned draft block (paper, section 3 "Models and
  * Protocol": an EAGLE-3 style drafter that also attends to the encoder output;
  * appendix "Draft architecture": the input mixes four target feature vectors with the

@@ -67,6 +67,7 @@ def _load():
         "ad_workspace_size": (_i32, [_ptr, _i32, _i32, _i32, ctypes.POINTER(_size)]),
         "ad_cross_kv_prefill": (_i32, [_ptr, _ptr, ctypes.POINTER(Cross), _ptr]),
         "ad_verify_step": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
+        "ad_verify_step_static": (_i32, [_ptr, ctypes.POINTER(Step), _ptr]),
         "ad_kv_commit": (_i32, [_ptr, _ptr, _i32, _ptr]),
         "ad_kv_commit_tree": (_i32, [_ptr, _ptr, _ptr, _ptr, _i32, _i32, _ptr]),
         "ad_anchordraft_loss_workspace_size": (_i32, [_ptr, _i32, _i32, ctypes.POINTER(_size)]),
@@ -94,7 +95,8 @@ def _load():
 LIB = _load()
 EXPORTS = ("ad_last_error", "ad_model_param_count", "ad_model_create", "ad_model_destroy",
            "ad_model_pack_size", "ad_model_pack",
-           "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_kv_commit", "ad_kv_commit_tree",
+           "ad_workspace_size", "ad_cross_kv_prefill", "ad_verify_step", "ad_verify_step_static",
+           "ad_kv_commit", "ad_kv_commit_tree",
            "ad_draft_heads_workspace_size", "ad_draft_heads", "ad_kv_import", "ad_kv_export",
            "ad_draft_input_workspace_size", "ad_draft_input",
            "ad_anchordraft_loss_workspace_size", "ad_anchordraft_loss",
@@ -191,6 +193,12 @@ def cross_kv_prefill(model: Model, enc, cross: Cross, stream=None):
 def verify_step(model: Model, step: Step, stream=None):
     check(LIB.ad_verify_step(model.handle, ctypes.byref(step), stream_handle(stream)),
           "ad_verify_step")
+
+
+def verify_step_static(model: Model, step: Step, stream=None):
+    """ad_verify_step in the library's static scratch (step.workspace is ignored)."""
+    check(LIB.ad_verify_step_static(model.handle, ctypes.byref(step), stream_handle(stream)),
+          "ad_verify_step_static")
 
 
 def kv_commit(kv_len, accept_len, batch: int, stream=None):

@@ -2,6 +2,7 @@
 // of kernel launches that makes one verify step.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -413,6 +414,32 @@ ad_status validate_desc(const ad_model_desc* d) {
   return AD_OK;
 }
 
+// Library-owned step scratch for callers that cannot allocate device memory
+// (ad_verify_step_static).  In host code `scratch` names a host-side stand-in, not a
+// device address: the device address of each GPU's copy comes from hipGetSymbolAddress,
+// taken once per device (with that device current) and kept in g_scratch_dev.
+constexpr size_t kStaticScratchBytes = AD_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+ad_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(AD_EHIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return fail(AD_EUNSUPPORTED, "device index past the static scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(AD_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return AD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -588,6 +615,22 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
   if (D.dtype == AD_BF16) run_step_mfma(model, s, w, st);
   else run_step_valu<ad::F32>(model, s, w, st);
   return check_hip("ad_verify_step");
+}
+
+ad_status ad_verify_step_static(const ad_model* model, const ad_step* s, void* stream) {
+  if (!model || !s) return fail(AD_EINVAL, "model or step is NULL");
+  if (s->rows <= 0 || s->batch < 1 || s->k_max < 0) return fail(AD_ERANGE, "rows, batch and k_max out of range");
+  const size_t need = carve(model->desc, s->rows, s->batch, s->k_max, nullptr).bytes;
+  if (need > kStaticScratchBytes)
+    return fail(AD_ENOSPACE, "this step needs " + std::to_string(need) + " bytes of scratch; the static scratch "
+                             "holds " + std::to_string(kStaticScratchBytes) + " (use ad_verify_step with a workspace)");
+  void* p = nullptr;
+  const ad_status rc = static_scratch(&p);
+  if (rc != AD_OK) return rc;
+  ad_step t = *s;
+  t.workspace = p;
+  t.workspace_bytes = kStaticScratchBytes;
+  return ad_verify_step(model, &t, stream);
 }
 
 // ad_draft_input's scratch.  float32 models: the gathered rows [B][4d], the feature

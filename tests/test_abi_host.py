@@ -164,3 +164,24 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert ad.LIB.ad_draft_heads(h, 0x1000, 0, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
                                  0x1000, ws.value, None) == -2
     ad.LIB.ad_model_destroy(h)
+
+
+def test_static_scratch_step_rejects_a_step_past_its_size(ad):
+    """ad_verify_step_static refuses a step whose scratch exceeds its static buffer
+    (the ragged batch of 64 at the large-v3 shape needs about 120 MiB) before anything is
+    enqueued, with a message naming the buffer."""
+    from paper_2608_12703_amd.configs import CONFIGS
+    cfg = CONFIGS["ragged_large_v3"]
+    n = ad.param_count(cfg)
+    fake = (ctypes.c_void_p * n)(*[256 * (i + 1) for i in range(n)])   # never dereferenced
+    h = ctypes.c_void_p()
+    assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, n, ctypes.byref(h)) == 0
+    need = ctypes.c_size_t()
+    assert ad.LIB.ad_workspace_size(h, 576, 64, 8, ctypes.byref(need)) == 0
+    assert need.value > 64 << 20
+    step = ad.Step()
+    step.batch, step.layout, step.k_max, step.rows = 64, ad.AD_PADDED, 8, 576
+    assert ad.LIB.ad_verify_step_static(h, ctypes.byref(step), None) == -3
+    assert b"static scratch" in ad.LIB.ad_last_error()
+    assert ad.LIB.ad_verify_step_static(None, ctypes.byref(step), None) == -1
+    ad.LIB.ad_model_destroy(h)
