@@ -61,8 +61,8 @@ def parse():
                    help="also time the AnchorDraft objective with its gradients at a training "
                         "batch of the draft (12 utterances x 128 positions)")
     p.add_argument("--graph", type=int, default=1,
-                   help="time the step replayed from a captured HIP graph (the eager time is "
-                        "reported beside it)")
+                   help="also time the step replayed from a captured HIP graph (reported beside "
+                        "the eager step, which is the headline)")
     p.add_argument("--workloads", type=int, default=1,
                    help="also measure the ragged batch (padded and packed), the drift-stress "
                         "loop and the tiny float32 model, and time the encoder K/V prefill")
@@ -130,7 +130,8 @@ def cpu_baseline(cfg, params, wl, n_seq=8):
     threads this process may use, then sequence 0's step again with one thread.  Each
     sequence's encoder K/V projection and the greedy continuation that plants its drafts
     are computed first and not timed, as on the GPU (they take about 6 s per sequence
-    at this shape, which is what bounds the sample)."""
+    at this shape, which is what bounds the sample).  The same steps are then timed
+    again with one BLAS thread."""
     from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import decoder as od
@@ -155,45 +156,37 @@ def cpu_baseline(cfg, params, wl, n_seq=8):
             rows += len(d) + 1
         timed = time.perf_counter() - t1
     with threadpool_limits(limits=1):
-        st, d = states[0]
         t2 = time.perf_counter()
-        r0 = od.verify(model, st, d)
+        for st, d in states:
+            od.verify(model, st, d)
         one = time.perf_counter() - t2
     return {"value": tokens / timed, "unit": "accepted tokens/s", "cores": int(used), "kind": "oracle",
             "cpu_model": cpu_model(),
-            "one_thread": {"value": (r0.accepted + 1) / one, "seconds": round(one, 2),
-                           "sample": "sequence 0's verify step"},
+            "one_thread": {"value": tokens / one, "seconds": round(one, 2), "sample": "the same steps"},
             "sample": f"the verify steps of sequences 0..{n_seq - 1} of the {wl.batch} (a quarter of the "
                       f"batch; {rows} rows, {tokens} tokens) in {timed:.1f} s with {used} BLAS threads "
                       f"(encoder K/V projection and draft planting, {setup:.1f} s, not timed)"}
 
 
 def copy_peaks(mib=1024, reps=5):
-    """Measured HBM rates on this GPU: a device copy of `mib` MiB (read + write bytes per
-    second) and a read-dominated reduction over the same buffer (bytes read per second)."""
+    """Measured HBM rate on this GPU: a device copy of `mib` MiB (read + write bytes per
+    second), the best of `reps`."""
     import torch
     n = (mib << 20) // 4
     src = torch.ones(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    best_c = best_r = 1e9
+    best_c = 1e9
     for _ in range(reps):
         ev0.record()
         dst.copy_(src)
         ev1.record()
         torch.cuda.synchronize()
         best_c = min(best_c, ev0.elapsed_time(ev1))
-        ev0.record()
-        _ = src.sum()
-        ev1.record()
-        torch.cuda.synchronize()
-        best_r = min(best_r, ev0.elapsed_time(ev1))
     nbytes = n * 4
     del src, dst
     return {"copy_GBps": round(2 * nbytes / (best_c / 1e3) / 1e9, 1),
-            "read_GBps": round(nbytes / (best_r / 1e3) / 1e9, 1),
-            "what": f"best of {reps}: device copy of {mib} MiB (read + write bytes) and a sum over it "
-                    f"(bytes read)"}
+            "what": f"best of {reps}: device copy of {mib} MiB, read + write bytes"}
 
 
 def time_prefill(sess, encs, reps=3):
@@ -439,7 +432,7 @@ def main():
     res2 = sess.results()
     assert np.array_equal(res2["accept_len"], res["accept_len"]), "steps were not repeatable"
     log(f"{ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f}), {tokens} tokens/step")
-    ms_eager = ms
+    ms_eager, ms_graph = ms, None
     if args.graph:
         # The same step (verify, commit, length reset) captured once into a HIP graph and
         # replayed: the same kernels with the same arguments, launched by the graph
@@ -457,12 +450,12 @@ def main():
             graph.replay()
         ev1.record(stream)
         torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1) / args.steps
+        ms_graph = ev0.elapsed_time(ev1) / args.steps
         res3 = sess.results()
         assert np.array_equal(res3["accept_len"], res["accept_len"])
         assert np.array_equal(res3["out_tokens"], res2["out_tokens"])
         assert np.array_equal(res3["hidden"].view(np.uint32), ref_hidden.view(np.uint32))
-        log(f"graph-launched: {ms:.3f} ms/step (eager {ms_eager:.3f})")
+        log(f"graph-launched: {ms_graph:.3f} ms/step (eager {ms_eager:.3f})")
         del graph
 
     sb = roofline.step_bytes(cfg, wl.n, wl.T, wl.k)
@@ -681,7 +674,7 @@ def main():
         log(f"tiny float32: {tiny['us_per_step']:.1f} us per verify step, "
             f"{tiny['us_per_round_end_to_end']:.1f} us per decode round")
         peaks = copy_peaks()
-        log(f"copy {peaks['copy_GBps']:.0f} GB/s, read {peaks['read_GBps']:.0f} GB/s")
+        log(f"device copy {peaks['copy_GBps']:.0f} GB/s")
     del encs
 
     if args.copy_calibration_mb:
@@ -717,8 +710,7 @@ def main():
         "unit": "accepted tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
-        "launch": "hip graph" if args.graph else "eager",
-        "eager_ms_per_step": round(ms_eager, 4),
+        "graph_ms_per_step": None if ms_graph is None else round(ms_graph, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": cfg.name, "batch": wl.batch, "k": int(wl.k.max()),
