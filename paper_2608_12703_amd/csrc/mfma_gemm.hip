@@ -3,7 +3,8 @@
 // C[m][n] = sum_k X[m][k] W[n][k] with W bf16 [N][K] and X float32 activations stored as
 // a hi/lo bf16 pair in A-fragment order.  A workgroup owns 128 output columns and up to
 // RTC 16-row tiles; its eight waves (two per SIMD, so one wave's LDS reads overlap the
-// other's matrix instructions) each own a quarter of the rows and half of the columns.
+// other's matrix instructions) each own a quarter of the rows and half of the columns
+// (with 8 row tiles: one row tile and all the columns each).
 // Weights (streamed from HBM) move in 32-wide K steps through an LDS ring filled by
 // direct global->LDS loads five steps ahead.  Activations (L2-resident) go straight into
 // a register ring five steps ahead for tiles of up to 8 row tiles (the A-fragment order
@@ -119,28 +120,34 @@ struct AFrag {
   uint4 h[RW], l[RW];
 };
 
-// One 32-wide K step with the activations from registers.
-template <int RTC>
-__device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RTC / 4][4], const AFrag<RTC / 4>& a,
+// One 32-wide K step with the activations from registers: RW row tiles x CT column
+// tiles (column group ch).
+template <int RW, int CT>
+__device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RW][CT], const AFrag<RW>& a,
                                              const uint4* wbuf, int ch, int lane) {
-  constexpr int RW = RTC / 4;
-  bf16x8 b[4];
+  bf16x8 b[CT];
 #pragma unroll
-  for (int ct = 0; ct < 4; ++ct) b[ct] = as_bf16x8(wbuf[(ch * 4 + ct) * 64 + lane]);
+  for (int ct = 0; ct < CT; ++ct) b[ct] = as_bf16x8(wbuf[(ch * CT + ct) * 64 + lane]);
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
     const bf16x8 ah = as_bf16x8(a.h[r]), al = as_bf16x8(a.l[r]);
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
       acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
       acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
     }
   }
 }
 
-template <int EPI, int RTC, bool PACKED, bool TWO = false>
+// WIDE (8 row tiles only): each wave owns one row tile and all 128 columns, so every
+// activation fragment is loaded once per workgroup (the default layout loads each one
+// twice, once per column half) and a K step does twice the matrix work for the same
+// operand bytes.  The order of every output's sums is the same in both layouts.
+template <int EPI, int RTC, bool PACKED, bool TWO = false, bool WIDE = false>
 __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
-  constexpr int RW = RTC / 4;            // row tiles per wave
+  static_assert(!WIDE || (RTC == 8 && EPI != EPI_ARGMAX), "the wide layout: 8 row tiles, no argmax");
+  constexpr int RW = WIDE ? 1 : RTC / 4;  // row tiles per wave
+  constexpr int CT = WIDE ? 8 : 4;        // 16-column tiles per wave
   constexpr int NA = RTC / 4;            // direct loads per wave for one activation stage
   // Activation ring: 3 stages (requested 2 steps ahead); weight ring: 6 stages (requested
   // 5 steps ahead, covering HBM latency).  Distinct LDS objects, so the compiler can tell
@@ -150,7 +157,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   __shared__ uint4 sa0[RTC * 128], sa1[RTC * 128], sa2[RTC * 128];
   __shared__ uint4 sw0[512], sw1[512], sw2[512], sw3[512], sw4[512], sw5[512];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int rg = w & 3, ch = w >> 2;     // row group, column half
+  const int rg = WIDE ? w : (w & 3), ch = WIDE ? 0 : (w >> 2);   // row group, column group
   const int c16 = lane & 15, grp = lane >> 4;
 
   // (split, column tile, row chunk) of this workgroup.  Workgroups are dealt
@@ -165,11 +172,11 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   const int rt0 = mc * RTC, n0 = nt * kNT;
   const int kb0 = (s * g.KB) / g.S, kb1 = ((s + 1) * g.KB) / g.S;
 
-  f32x4 acc[RW][4];
+  f32x4 acc[RW][CT];
 #pragma unroll
   for (int r = 0; r < RW; ++r)
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ct = 0; ct < CT; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = kb1 - kb0, kl = kb1 - 1;
   auto ia = [&](uint4* buf, int kb) {   // activation stage of step kb (clamped)
@@ -230,8 +237,8 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
       iw(NW0, kb + 4);                                            \
       la(NA1, kb + 5);                                            \
       iw(NW1, kb + 5);                                            \
-      mma_step_reg<RTC>(acc, CA0, CW0, ch, lane);                 \
-      if (kb + 1 < kb1) mma_step_reg<RTC>(acc, CA1, CW1, ch, lane);\
+      mma_step_reg<RW, CT>(acc, CA0, CW0, ch, lane);                 \
+      if (kb + 1 < kb1) mma_step_reg<RW, CT>(acc, CA1, CW1, ch, lane);\
       BARRIER_VMCNT(kWait2);                                      \
       kb += 2;                                                    \
     }
@@ -261,7 +268,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     {                                               \
       la(NXA, kb + 5);                              \
       iw(NXW, kb + 5);                              \
-      mma_step_reg<RTC>(acc, CA, CW, ch, lane);     \
+      mma_step_reg<RW, CT>(acc, CA, CW, ch, lane);  \
       BARRIER_VMCNT(kWait);                         \
       ++kb;                                         \
     }
@@ -322,7 +329,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
 
   // row / column of accumulator element (r, ct, i) of this lane
   const int row_base = (rt0 + rg * RW) * 16 + grp * 4;   // + r * 16 + i
-  const int col_base = n0 + ch * 64 + c16;               // + ct * 16
+  const int col_base = n0 + ch * CT * 16 + c16;          // + ct * 16
 
   // This kernel's LDS is also written by direct loads, so the compiler orders every LDS
   // access after outstanding global stores; epilogues therefore finish all their
@@ -376,9 +383,9 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   if (EPI == EPI_GELU) {
     // FFN up-projection (unsplit): bias + GELU, stored straight from registers as the
     // next product's A operand (hi/lo bf16 pair in A-fragment order)
-    float bv[4];
+    float bv[CT];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
       const int n = min(col_base + ct * 16, g.N - 1);
       bv[ct] = bf16_to_f32(g.bias[n]);
     }
@@ -389,7 +396,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
         const int m = row_base + r * 16 + i;
         if (m >= g.M) continue;
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
+        for (int ct = 0; ct < CT; ++ct) {
           const int n = col_base + ct * 16;
           if (n < g.N) afrag_store(g.e.frag, g.e.frag_RT, m, n, gelu_erf(acc[r][ct][i] + bv[ct]));
         }
@@ -408,7 +415,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
       const int m = row_base + r * 16 + i;
       if (m >= g.M) continue;
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct) {
+      for (int ct = 0; ct < CT; ++ct) {
         const int n = col_base + ct * 16;
         if (n < g.N) __builtin_nontemporal_store(acc[r][ct][i], &P[(size_t)m * g.N + n]);
       }
@@ -452,8 +459,12 @@ __global__ void __launch_bounds__(64) argmax_final_kernel(int M, int nrec, const
 
 // Launch planning.  A workgroup's time is dominated by fixed costs (first-load latency,
 // the partial stores) plus its K steps, and a second round of workgroups costs a whole
-// extra pass, so plans keep the grid within one workgroup per CU.  Measured per-step
-// times for 4 / 8 / 16 row tiles: about 0.27 / 0.43 / 0.8 us.
+// extra pass, so plans keep the grid within one workgroup per CU.  Per-step times for
+// 4 / 8 / 16 row tiles: about 0.27 / 0.43 / 0.8 us.  (The wide 8-row-tile layout runs a
+// step in about 0.38 us alone; priced that way, the 1280 x 5120 down-projection would
+// take 12 splits instead of 6, which is faster alone (9.7 against 13.3 us) but slower
+// inside the verify step (4.978 against 4.952 ms), where the consumer sums twice the
+// partials.)
 constexpr int kMaxWGs = 256;
 constexpr int kRefRows = 224;   // reference block for the split choice (32 sequences x 7 rows)
 
@@ -513,12 +524,18 @@ int lm_records(int V) { return 2 * ((V + kNT - 1) / kNT); }
 // tile's sums.
 constexpr int kTwoStepMin = 24;
 
+// Eight row tiles always take the wide wave layout, except for the LM head's argmax
+// epilogue, which merges per column half.  Alone, the wide loop measured as fast or faster
+// on every projection shape (the 1280 x 5120 down-projection at 224 rows, 12 splits: 9.7
+// against 14.0 us); the 64-sequence ragged batch padded to 576 rows, whose projections
+// take 8 row tiles, runs its verify step in 7.77 ms against 8.26 ms.
 template <int EPI, int RTC, bool PACKED>
 static void launch_rtc(const GemmArgs& g, dim3 grid, hipStream_t st) {
+  constexpr bool kWide = RTC == 8 && EPI != EPI_ARGMAX;
   if (RTC <= 8 && g.KB / g.S >= kTwoStepMin)
-    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, RTC <= 8>), grid, dim3(512), 0, st, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, RTC <= 8, kWide>), grid, dim3(512), 0, st, g);
   else
-    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, false>), grid, dim3(512), 0, st, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<EPI, RTC, PACKED, false, kWide>), grid, dim3(512), 0, st, g);
 }
 
 template <int EPI>
