@@ -42,14 +42,17 @@ const void* lp(const ad_model* m, int layer, int which) {
   return m->p[4 + layer * N_LAYER_PARAMS + which];
 }
 
-// Tiled-weight buffer: per layer W_QKV, W_O, W_XQ, W_XO, W_1, W_2, then the LM head.
-constexpr int kPackedPerLayer = 6;
-const int kPackedWhich[kPackedPerLayer] = {W_QKV, W_O, W_XQ, W_XO, W_1, W_2};
+// Tiled-weight buffer: per layer W_QKV, W_O, W_XQ, W_XO, W_1, W_2 and the encoder K/V
+// projection W_XKV (read by the prefill), then the LM head.
+constexpr int kPackedPerLayer = 7;
+const int kPackedWhich[kPackedPerLayer] = {W_QKV, W_O, W_XQ, W_XO, W_1, W_2, W_XKV};
+constexpr int kPackedXkv = 6;   // slot of W_XKV
 
 void packed_shape(const ad_model_desc& D, int which, int& N, int& K) {
   const int d = D.d_model, F = D.d_ffn;
   N = d; K = d;
   if (which == W_QKV) N = 3 * d;
+  if (which == W_XKV) N = 2 * d;
   if (which == W_1) N = F;
   if (which == W_2) K = F;
 }
@@ -867,13 +870,26 @@ ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_c
   e.d = D.d_model;
   e.frames_cap = cross->frames_cap;
   // bf16 models: the matrix cores (a large dense product); float32 models: the VALU.
+  // With two or more layers the bf16 path first copies the encoder states into fragment
+  // order, staged in the last layer's part of the cache (frames_cap x 2d elements, at
+  // least the frames_cap x d of the copy), which is only written by the last launch;
+  // that launch reads the row-major states.  A tiled model supplies tiled weights.
+  const bool stage = D.dtype == AD_BF16 && D.n_layers >= 2;
+  const size_t layer_elems = (size_t)2 * D.n_heads * cross->frames_cap * 64;
+  uint16_t* staged = (uint16_t*)cross->data + (size_t)(D.n_layers - 1) * layer_elems;
+  if (stage) ad::launch_pack_rows((const uint16_t*)enc, cross->frames_cap, D.d_model, staged, st);
   for (int l = 0; l < D.n_layers; ++l) {
     e.layer = l;
-    if (D.dtype == AD_BF16)
-      ad::launch_xkv_mfma(cross->frames_cap, 2 * D.d_model, D.d_model, (const uint16_t*)enc,
-                          (const uint16_t*)lp(model, l, W_XKV), (const uint16_t*)lp(model, l, B_XKV),
-                          (uint16_t*)cross->data, l, D.n_heads, D.d_model, cross->frames_cap, st);
-    else
+    if (D.dtype == AD_BF16) {
+      const bool a_packed = stage && l < D.n_layers - 1;
+      const bool w_packed = model->packed != nullptr;
+      const uint16_t* W = w_packed ? model->packed + model->pack_off[l * kPackedPerLayer + kPackedXkv]
+                                   : (const uint16_t*)lp(model, l, W_XKV);
+      ad::launch_xkv_mfma(cross->frames_cap, 2 * D.d_model, D.d_model,
+                          a_packed ? staged : (const uint16_t*)enc, a_packed, W, w_packed,
+                          (const uint16_t*)lp(model, l, B_XKV), (uint16_t*)cross->data, l, D.n_heads,
+                          D.d_model, cross->frames_cap, st);
+    } else
       ad::launch_gemm_valu<ad::F32>(ad::EPI_XKV, cross->frames_cap, 2 * D.d_model, D.d_model,
                                     (const float*)enc, lp(model, l, W_XKV), lp(model, l, B_XKV), e, st);
   }

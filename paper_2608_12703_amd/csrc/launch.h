@@ -89,9 +89,15 @@ void launch_gemm_valu(int epi, int M, int N, int K, const float* A, const void* 
                       const EpiArgs& e, hipStream_t st);
 
 // Cross-attention keys / values of a bf16 model's encoder states on the matrix cores:
-// cache <- enc [M][K] W [N][K]^T + bias in the cross-K/V layout of `layer` (N = 2d).
-void launch_xkv_mfma(int M, int N, int K, const uint16_t* A, const uint16_t* W, const uint16_t* bias,
-                     uint16_t* cache, int layer, int H, int d, int frames_cap, hipStream_t st);
+// cache <- enc [M][K] W [N][K]^T + bias in the cross-K/V layout of `layer` (N = 2d, M a
+// multiple of 32).  a_packed: enc as written by launch_pack_rows; w_packed: W tiled by
+// launch_pack_weight; otherwise row-major.
+void launch_xkv_mfma(int M, int N, int K, const uint16_t* A, bool a_packed, const uint16_t* W,
+                     bool w_packed, const uint16_t* bias, uint16_t* cache, int layer, int H, int d,
+                     int frames_cap, hipStream_t st);
+// Row-major bf16 [M][K] (M a multiple of 16, K of 32) into the fragment order the
+// prefill reads (M * K elements).
+void launch_pack_rows(const uint16_t* A, int M, int K, uint16_t* P, hipStream_t st);
 
 // bf16 matrix-core product: X (A-fragment order, RT row tiles, RT a multiple of 16)
 // times W^T.

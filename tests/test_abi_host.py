@@ -66,8 +66,9 @@ def test_param_count_and_model_validation(ad):
     assert ad.LIB.ad_model_create(ctypes.byref(ad.model_desc(cfg)), fake, 44, ctypes.byref(h)) == 0
     n = ctypes.c_size_t()
     assert ad.LIB.ad_model_pack_size(h, ctypes.byref(n)) == 0
-    # per layer 6 tiled matrices, then the LM head: N rounded up to 128 columns
-    want = 2 * (2 * (384 * 128 + 128 * 128 * 3 + 256 * 128 + 128 * 256) + 128 * 128)
+    # per layer 7 tiled matrices (QKV, O, cross-Q, cross-O, FFN up and down, encoder K/V),
+    # then the LM head: N rounded up to 128 columns
+    want = 2 * (2 * (384 * 128 + 128 * 128 * 3 + 256 * 128 + 128 * 256 + 256 * 128) + 128 * 128)
     assert n.value == want
     assert ad.LIB.ad_model_pack(h, 0x1008, n.value, None) == -1      # misaligned
     assert ad.LIB.ad_model_pack(h, 0x1000, n.value - 1, None) == -3  # too small

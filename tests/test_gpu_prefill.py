@@ -3,7 +3,7 @@ audio at every step) against the oracle's projection, value by value.
 
 K_l = enc W_k,l^T and V_l = enc W_v,l^T + b_v,l in float64, rounded to bf16, against the
 cache the matrix-core prefill writes (decoded from the cache's 32-frame block layout).
-Both sides round the same 1280-term sum (float32 matrix accumulation on the GPU, float64
+Both sides round the same d-term sum (float32 matrix accumulation on the GPU, float64
 in the oracle) to bf16.  The two sums differ by ~1e-6 of the values' rms (an error that
 scales with the terms, so a value near zero may lie several of its own ulps away), far
 below an ulp of 2^-8..2^-7 of a typical value: a value differs only when the sums
@@ -23,11 +23,11 @@ from gpu_common import EPS_OWN, KV_SIGMAS, decode_cross
 pytestmark = pytest.mark.gpu
 
 
-def _check(cfg, frames, layers, seq_ids=None):
+def _check(cfg, frames, layers, seq_ids=None, pack_weights=True):
     params = synth.make_params(cfg)
     B = len(frames)
     ids = list(range(B)) if seq_ids is None else seq_ids
-    sess = Session(cfg, params, B, 0, frames)
+    sess = Session(cfg, params, B, 0, frames, pack_weights=pack_weights)
     encs = [synth.make_encoder(cfg, ids[b], frames[b]) for b in range(B)]
     sess.prefill_encoder(encs)
     flat = sess.cross.float().cpu().numpy()
@@ -63,6 +63,17 @@ def test_prefill_matches_oracle_small(dtype):
                  dtype=dtype, batch=3, k=1, frames=300, seed=5)
     # ragged lengths: tails inside a 32-frame block and inside a 256-frame tile
     _check(cfg, [300, 37, 129], layers=[0, 1])
+
+
+@pytest.mark.parametrize("pack_weights", [True, False])
+@pytest.mark.parametrize("n_layers", [1, 3])
+def test_prefill_operand_layouts(pack_weights, n_layers):
+    """Tiled and row-major weights; one layer (the encoder states are read row-major) and
+    three (the first two read them in fragment order, staged in the last layer's cache).
+    d 512: whole 256-column key and value tiles (the 8-byte stores) next to a frame tail."""
+    cfg = Config(name="unit_prefill_layout", n_layers=n_layers, d_model=512, n_heads=8, d_ffn=1024,
+                 vocab=1000, dtype="bf16", batch=2, k=1, frames=600, seed=9)
+    _check(cfg, [600, 211], layers=list(range(n_layers)), pack_weights=pack_weights)
 
 
 def test_prefill_matches_oracle_large_v3():
