@@ -110,7 +110,8 @@ ad_status ad_model_destroy(ad_model* model);
 /*
  * Optional weight tiling for the bf16 matrix-core path.  ad_model_pack_size gives the
  * bytes of a caller-allocated device buffer; ad_model_pack fills it with a tiled copy of
- * every projection matrix and of the tied LM head (for each 128-column tile and 32-wide
+ * every projection matrix (the encoder K/V projection included) and of the tied LM
+ * head (for each 128-column tile and 32-wide
  * K step, one contiguous 8 KB block in the order the kernels stage it) and makes the
  * model read its weights from there.  The buffer must stay allocated and unchanged while
  * the model is used; pack again after changing the parameters.  buffer = NULL returns
@@ -231,6 +232,9 @@ ad_status ad_workspace_size(const ad_model* model, int32_t max_rows, int32_t max
  * (the decoder reuses the encoded audio at every step; paper, section 1 and appendix
  * "Draft architecture").  enc is device [frames_cap][d] of the model dtype, sequence b
  * at rows enc_off[b].. (rows outside any sequence are projected too and never read).
+ * cross->data is written only; with two or more layers its last layer's part also
+ * serves as scratch for a copy of enc (bf16 models) before that layer is written, so
+ * enc must not lie inside it.  A tiled model (ad_model_pack) reads its tiled weights.
  * Errors: AD_EINVAL, AD_ERANGE (frames_cap not a positive multiple of 32).
  */
 ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_cross* cross,

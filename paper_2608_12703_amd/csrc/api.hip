@@ -877,6 +877,11 @@ ad_status ad_cross_kv_prefill(const ad_model* model, const void* enc, const ad_c
   const bool stage = D.dtype == AD_BF16 && D.n_layers >= 2;
   const size_t layer_elems = (size_t)2 * D.n_heads * cross->frames_cap * 64;
   uint16_t* staged = (uint16_t*)cross->data + (size_t)(D.n_layers - 1) * layer_elems;
+  if (stage) {
+    const uintptr_t e0 = (uintptr_t)enc, e1 = e0 + (size_t)cross->frames_cap * D.d_model * 2;
+    const uintptr_t s0 = (uintptr_t)staged, s1 = s0 + layer_elems * 2;
+    if (e0 < s1 && s0 < e1) return fail(AD_EINVAL, "enc overlaps the last layer's cross-K/V slots");
+  }
   if (stage) ad::launch_pack_rows((const uint16_t*)enc, cross->frames_cap, D.d_model, staged, st);
   for (int l = 0; l < D.n_layers; ++l) {
     e.layer = l;

@@ -158,6 +158,11 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert ad.LIB.ad_kv_export(h, ctypes.byref(kv), -1, 0x1000, 3, 0x1000, None) == -2
     cross = ad.Cross(0x1000, 17, 0x1000, 0x1000)
     assert ad.LIB.ad_cross_kv_prefill(h, 0x1000, ctypes.byref(cross), None) == -2
+    # encoder states inside the last layer's slots (its prefill scratch) are refused
+    cross = ad.Cross(0x100000, 64, 0x1000, 0x1000)
+    last = 0x100000 + (cfg.n_layers - 1) * 2 * cfg.n_heads * 64 * 64 * 2
+    assert ad.LIB.ad_cross_kv_prefill(h, last + 256, ctypes.byref(cross), None) == -1
+    assert b"overlaps" in ad.LIB.ad_last_error()
     ws = ctypes.c_size_t()
     assert ad.LIB.ad_draft_heads_workspace_size(h, 4, 1, ctypes.byref(ws)) == 0
     assert ad.LIB.ad_draft_heads(h, 0x1000, 4, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
