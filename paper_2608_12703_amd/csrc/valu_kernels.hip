@@ -9,37 +9,123 @@
 namespace ad {
 
 // ---------------------------------------------------------------- GEMM
-// C[m][n] = sum_k A[m][k] W[n][k] (+ bias[n]); 32 x 64 output tile per 256 threads.
+// C[m][n] = sum_k A[m][k] W[n][k] (+ bias[n]); 32 x 64 output tile per 256 threads, K in
+// steps of 32 (K a multiple of 32).  Each output is one thread's fma chain over k in
+// order.  A step's operands pass through LDS; every thread requests its slice of the
+// operands kVStages steps ahead into registers, so a workgroup's K loop waits for memory
+// once rather than once per step (with few rows, as in batch-1 decoding, the loop is
+// otherwise a chain of dependent round trips).
+
+constexpr int kVStages = 8;
+
+// One thread's slice of a K step: 4 activations of row ar; 8 weights (4 of rows wr and
+// wr + 32 in float32, or 8 of row wb in bf16).
+template <class S>
+struct VStage;
+template <>
+struct VStage<F32> {
+  float4 a, w0, w1;
+};
+template <>
+struct VStage<BF16> {
+  float4 a;
+  uint4 w;
+};
+
+template <class S>
+__device__ __forceinline__ void vstage_load(VStage<S>& st, int kb, int M, int N, int K, const float* A,
+                                            const typename S::T* W, int m0, int n0, int tid) {
+  const int k0 = kb * 32;
+  const bool kin = k0 < K;
+  const int ar = tid >> 3, ak = (tid & 7) * 4;
+  const int m = m0 + ar;
+  st.a = (kin && m < M) ? *(const float4*)(A + (size_t)m * K + k0 + ak) : float4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (sizeof(typename S::T) == 4) {
+    const int wr = tid >> 3, wk = (tid & 7) * 4;
+    const int n1 = n0 + wr, n2 = n0 + wr + 32;
+    st.w0 = (kin && n1 < N) ? *(const float4*)(W + (size_t)n1 * K + k0 + wk) : float4{0.f, 0.f, 0.f, 0.f};
+    st.w1 = (kin && n2 < N) ? *(const float4*)(W + (size_t)n2 * K + k0 + wk) : float4{0.f, 0.f, 0.f, 0.f};
+  } else {
+    const int wb = tid >> 2, wk = (tid & 3) * 8;
+    const int n = n0 + wb;
+    st.w = (kin && n < N) ? *(const uint4*)(W + (size_t)n * K + k0 + wk) : make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <class S>
+__device__ __forceinline__ void vstage_put(const VStage<S>& st, float (*As)[33], float (*Ws)[33], int tid) {
+  const int ar = tid >> 3, ak = (tid & 7) * 4;
+  As[ar][ak + 0] = st.a.x;
+  As[ar][ak + 1] = st.a.y;
+  As[ar][ak + 2] = st.a.z;
+  As[ar][ak + 3] = st.a.w;
+  if constexpr (sizeof(typename S::T) == 4) {
+    const int wr = tid >> 3, wk = (tid & 7) * 4;
+    Ws[wr][wk + 0] = st.w0.x;
+    Ws[wr][wk + 1] = st.w0.y;
+    Ws[wr][wk + 2] = st.w0.z;
+    Ws[wr][wk + 3] = st.w0.w;
+    Ws[wr + 32][wk + 0] = st.w1.x;
+    Ws[wr + 32][wk + 1] = st.w1.y;
+    Ws[wr + 32][wk + 2] = st.w1.z;
+    Ws[wr + 32][wk + 3] = st.w1.w;
+  } else {
+    const int wb = tid >> 2, wk = (tid & 3) * 8;
+    const uint32_t u[4] = {st.w.x, st.w.y, st.w.z, st.w.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      Ws[wb][wk + 2 * j] = bf16_to_f32(u[j] & 0xffff);
+      Ws[wb][wk + 2 * j + 1] = bf16_to_f32(u[j] >> 16);
+    }
+  }
+}
 
 template <class S, class SA, int EPI>
 __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, const typename SA::T* A,
                                                         const typename S::T* W,
                                                         const typename S::T* bias, EpiArgs e) {
+  static_assert(sizeof(typename SA::T) == 4, "float32 activations");
   __shared__ float As[32][33];
   __shared__ float Ws[64][33];
   const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
   const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 64;
+  const int KB = K / 32;
   float acc[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) acc[r] = 0.f;
-  for (int k0 = 0; k0 < K; k0 += 32) {
-    for (int i = tid; i < 32 * 32; i += 256) {
-      const int r = i >> 5, c = i & 31, m = m0 + r, k = k0 + c;
-      As[r][c] = (m < M && k < K) ? SA::ld(A, (size_t)m * K + k) : 0.f;
-    }
-    for (int i = tid; i < 64 * 32; i += 256) {
-      const int r = i >> 5, c = i & 31, n = n0 + r, k = k0 + c;
-      Ws[r][c] = (n < N && k < K) ? S::ld(W, (size_t)n * K + k) : 0.f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < 32; ++kk) {
-      const float w = Ws[tx][kk];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) acc[r] = fmaf(As[ty * 8 + r][kk], w, acc[r]);
-    }
-    __syncthreads();
+  VStage<S> s0, s1, s2, s3, s4, s5, s6, s7;
+  vstage_load<S>(s0, 0, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s1, 1, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s2, 2, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s3, 3, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s4, 4, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s5, 5, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s6, 6, M, N, K, A, W, m0, n0, tid);
+  vstage_load<S>(s7, 7, M, N, K, A, W, m0, n0, tid);
+  // step kb: stage its operands in LDS, multiply, request step kb + kVStages into the
+  // freed registers
+#define VGEMM_STEP(ST, J)                                                 \
+  if (kb + (J) < KB) {                                                    \
+    __syncthreads();                                                      \
+    vstage_put<S>(ST, As, Ws, tid);                                       \
+    __syncthreads();                                                      \
+    _Pragma("unroll 8") for (int kk = 0; kk < 32; ++kk) {                 \
+      const float w = Ws[tx][kk];                                         \
+      _Pragma("unroll") for (int r = 0; r < 8; ++r) acc[r] = fmaf(As[ty * 8 + r][kk], w, acc[r]); \
+    }                                                                     \
+    vstage_load<S>(ST, kb + (J) + kVStages, M, N, K, A, W, m0, n0, tid);  \
   }
+  for (int kb = 0; kb < KB; kb += kVStages) {
+    VGEMM_STEP(s0, 0)
+    VGEMM_STEP(s1, 1)
+    VGEMM_STEP(s2, 2)
+    VGEMM_STEP(s3, 3)
+    VGEMM_STEP(s4, 4)
+    VGEMM_STEP(s5, 5)
+    VGEMM_STEP(s6, 6)
+    VGEMM_STEP(s7, 7)
+  }
+#undef VGEMM_STEP
   const int n = n0 + tx;
   if (n >= N) return;
   const float bn = bias ? S::ld(bias, n) : 0.f;
@@ -102,7 +188,93 @@ template void launch_gemm_valu<BF16>(int, int, int, int, const float*, const voi
 // One block per (head, sequence).  Queries are taken 16 at a time; keys stream through
 // LDS in chunks of 64 at absolute positions 0, 64, 128, ... with an online softmax per
 // query.  A key a query may not see contributes exp(-inf) = 0; keys past every query's
-// range are staged as zeros so stale cache slots never reach the output.
+// range are staged as zeros so stale cache slots never reach the output.  Every thread
+// requests its part of a chunk (two runs of 8 keys' lanes and two runs of 8 values of
+// one lane, contiguous in both cache layouts) kAStages chunks ahead into registers.
+
+constexpr int kAStages = 4;
+
+template <class S>
+struct AStage;
+template <>
+struct AStage<F32> {
+  float4 k[2][2], v[2][2];
+};
+template <>
+struct AStage<BF16> {
+  uint4 k[2], v[2];
+};
+
+// Load chunk c0 (keys c0 .. c0 + 63): piece u of this thread is key run (key tid / 8 +
+// 32 u, lanes 8 (tid % 8) ..) and value run (lane tid / 8 + 32 u, keys c0 + 8 (tid % 8) ..).
+// Keys at or past n_keys read as zeros; a chunk at or past n_keys issues no loads.
+template <class S, bool CROSS>
+__device__ __forceinline__ void astage_load(AStage<S>& st, int c0, int n_keys, int layer, int h, int H,
+                                            int b, const SeqDesc& s, const typename S::T* kv,
+                                            int num_pages, const int* block_table, int pages_per_seq,
+                                            int frames_cap, int tid) {
+  constexpr bool F = sizeof(typename S::T) == 4;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int tk = c0 + (tid >> 3) + 32 * u, jk = (tid & 7) * 8;   // key run
+    const int jv = (tid >> 3) + 32 * u, tv = c0 + (tid & 7) * 8;   // value run
+    size_t bk = 0, bv = 0;
+    if (CROSS) {
+      bk = cross_base(layer, h, H, frames_cap) + cross_off(0, s.enc_off + min(tk, n_keys - 1), jk);
+      bv = cross_base(layer, h, H, frames_cap) + cross_off(1, s.enc_off + min(tv, n_keys - 1) / 8 * 8, jv);
+    } else {
+      const int pk = min(max(block_table[(size_t)b * pages_per_seq + min(tk, n_keys - 1) / kTile], 0), num_pages - 1);
+      const int pv = min(max(block_table[(size_t)b * pages_per_seq + min(tv, n_keys - 1) / kTile], 0), num_pages - 1);
+      bk = kv_tile_base(layer, 0, pk, h, num_pages, H) + tile_off(0, min(tk, n_keys - 1) % kTile, jk);
+      bv = kv_tile_base(layer, 1, pv, h, num_pages, H) + tile_off(1, min(tv, n_keys - 1) / 8 * 8 % kTile, jv);
+    }
+    const bool kin = tk < n_keys, vin = tv < n_keys;
+    if constexpr (F) {
+      const float4 z{0.f, 0.f, 0.f, 0.f};
+      st.k[u][0] = kin ? *(const float4*)(kv + bk) : z;
+      st.k[u][1] = kin ? *(const float4*)(kv + bk + 4) : z;
+      st.v[u][0] = vin ? *(const float4*)(kv + bv) : z;
+      st.v[u][1] = vin ? *(const float4*)(kv + bv + 4) : z;
+    } else {
+      st.k[u] = kin ? *(const uint4*)(kv + bk) : make_uint4(0, 0, 0, 0);
+      st.v[u] = vin ? *(const uint4*)(kv + bv) : make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
+// Chunk c0's registers into LDS: ks[key][lane], vs[key][lane]; value slots at or past
+// n_keys are zeroed.
+template <class S>
+__device__ __forceinline__ void astage_put(const AStage<S>& st, int c0, int n_keys, float (*ks)[65],
+                                           float (*vs)[65], int tid) {
+  constexpr bool F = sizeof(typename S::T) == 4;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int rk = (tid >> 3) + 32 * u, jk = (tid & 7) * 8;
+    const int jv = (tid >> 3) + 32 * u, rv = (tid & 7) * 8;
+    float kx[8], vx[8];
+    if constexpr (F) {
+      const float4 a = st.k[u][0], bq = st.k[u][1], c = st.v[u][0], dq = st.v[u][1];
+      kx[0] = a.x; kx[1] = a.y; kx[2] = a.z; kx[3] = a.w; kx[4] = bq.x; kx[5] = bq.y; kx[6] = bq.z; kx[7] = bq.w;
+      vx[0] = c.x; vx[1] = c.y; vx[2] = c.z; vx[3] = c.w; vx[4] = dq.x; vx[5] = dq.y; vx[6] = dq.z; vx[7] = dq.w;
+    } else {
+      const uint32_t ku[4] = {st.k[u].x, st.k[u].y, st.k[u].z, st.k[u].w};
+      const uint32_t vu[4] = {st.v[u].x, st.v[u].y, st.v[u].z, st.v[u].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        kx[2 * j] = bf16_to_f32(ku[j] & 0xffff);
+        kx[2 * j + 1] = bf16_to_f32(ku[j] >> 16);
+        vx[2 * j] = bf16_to_f32(vu[j] & 0xffff);
+        vx[2 * j + 1] = bf16_to_f32(vu[j] >> 16);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ks[rk][jk + e] = kx[e];
+      vs[rv + e][jv] = (c0 + rv + e < n_keys) ? vx[e] : 0.f;
+    }
+  }
+}
 
 template <class S, bool CROSS>
 __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
@@ -133,29 +305,19 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
     const unsigned long long tm = (!CROSS && qi < nq) ? tree[s.row0 + qg + qi].mask : 0ull;
     const int n_keys = CROSS ? s.whi : s.n + qg + nq;
     float m_run = -INFINITY, l_run = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = lo / 64 * 64; c0 < n_keys; c0 += 64) {
-      __syncthreads();
-      for (int i = tid; i < 64 * 64; i += 256) {
-        const int key = i >> 6, j = i & 63, t = c0 + key;
-        float kk = 0.f, vv = 0.f;
-        if (t < n_keys) {
-          size_t bk, bv;
-          if (CROSS) {
-            bk = cross_base(layer, h, H, frames_cap) + cross_off(0, s.enc_off + t, j);
-            bv = cross_base(layer, h, H, frames_cap) + cross_off(1, s.enc_off + t, j);
-          } else {
-            int pg = block_table[(size_t)b * pages_per_seq + t / kTile];
-            pg = min(max(pg, 0), num_pages - 1);
-            bk = kv_tile_base(layer, 0, pg, h, num_pages, H) + tile_off(0, t % kTile, j);
-            bv = kv_tile_base(layer, 1, pg, h, num_pages, H) + tile_off(1, t % kTile, j);
-          }
-          kk = S::ld(kv, bk);
-          vv = S::ld(kv, bv);
-        }
-        ks[key][j] = kk;
-        vs[key][j] = vv;
-      }
-      __syncthreads();
+    const int c_first = lo / 64 * 64, nch = n_keys > c_first ? (n_keys - c_first + 63) / 64 : 0;
+    AStage<S> st0, st1, st2, st3;
+    auto load = [&](AStage<S>& st, int ci) {
+      if (ci < nch)
+        astage_load<S, CROSS>(st, c_first + ci * 64, n_keys, layer, h, H, b, s, kv, num_pages, block_table,
+                              pages_per_seq, frames_cap, tid);
+    };
+    load(st0, 0);
+    load(st1, 1);
+    load(st2, 2);
+    load(st3, 3);
+    // the scores, the online-softmax update and the value product of chunk c0 (in LDS)
+    auto attend = [&](int c0) __attribute__((always_inline)) {
       float sc[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -192,7 +354,25 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[r] = fmaf(p, vs[key][part * 4 + r], o[r]);
       }
+    };
+    // chunk ci of the ring slot ST: stage it in LDS, request chunk ci + kAStages into the
+    // freed registers, attend
+#define VATT_CHUNK(ST, J)                                  \
+  if (ci + (J) < nch) {                                    \
+    const int c0 = c_first + (ci + (J)) * 64;              \
+    __syncthreads();                                       \
+    astage_put<S>(ST, c0, n_keys, ks, vs, tid);            \
+    load(ST, ci + (J) + kAStages);                         \
+    __syncthreads();                                       \
+    attend(c0);                                            \
+  }
+    for (int ci = 0; ci < nch; ci += kAStages) {
+      VATT_CHUNK(st0, 0)
+      VATT_CHUNK(st1, 1)
+      VATT_CHUNK(st2, 2)
+      VATT_CHUNK(st3, 3)
     }
+#undef VATT_CHUNK
     if (qi < nq) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)

@@ -90,6 +90,9 @@ def traffic(fetch_db: str, write_db: str, kernel: str, calib_mib: int, command: 
             "command": command}
 
 
+N_XCD, N_SIMD = 8, 1024
+
+
 def counter_table(dbs, kernels=None) -> str:
     """Mean value per dispatch of each counter, per kernel name (matching `kernels`)."""
     from .roofline import BF16_MFMA_PEAK
@@ -128,6 +131,17 @@ def counter_table(dbs, kernels=None) -> str:
             rate = flops / (mean_ns * 1e-9)
             out.append(f"    bf16 matrix work {flops / 1e9:.2f} GFLOP per dispatch -> {rate / 1e12:.1f} TFLOP/s "
                        f"= {100 * rate / BF16_MFMA_PEAK:.1f}% of the dense bf16 peak")
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in cs and "GRBM_GUI_ACTIVE" in cs and mean_ns:
+            # GRBM_GUI_ACTIVE sums the 8 XCDs over the counter window (the dispatch plus a
+            # few microseconds around it: a lower bound on the busy fraction of a short
+            # kernel); the busy cycles sum the 1024 SIMDs (256 CUs x 4)
+            busy = cs["SQ_VALU_MFMA_BUSY_CYCLES"][0] / cs["SQ_VALU_MFMA_BUSY_CYCLES"][1]
+            xcd_cycles = cs["GRBM_GUI_ACTIVE"][0] / cs["GRBM_GUI_ACTIVE"][1] / N_XCD
+            out.append(f"    matrix pipes busy {100 * busy / (xcd_cycles * N_SIMD):.1f}% of the SIMD cycles of "
+                       f"the counter window ({xcd_cycles:.0f} cycles per XCD)")
+        if "SQ_WAIT_INST_ANY" in cs and "SQ_WAVE_CYCLES" in cs:
+            wait = cs["SQ_WAIT_INST_ANY"][0] / max(cs["SQ_WAVE_CYCLES"][0], 1.0)
+            out.append(f"    waves waiting on a dependency {100 * wait:.1f}% of their cycles")
     return "\n".join(out)
 
 

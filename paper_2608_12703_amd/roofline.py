@@ -51,10 +51,12 @@ def step_flops(cfg, n, T, k) -> dict:
             "attention": int(np.sum(4 * (k + 1) * (T + n + k + 1) * d * L))}
 
 
-# Sources the cross-attention kernel is built from; HBM counter figures taken for one
-# version of them are reported only while they are unchanged.
+# Sources the cross-attention kernel is built from (its file, the shared device helpers
+# and the declaration of its argument struct); HBM counter figures taken for one version
+# of them are reported only while they are unchanged.
 _CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
-KERNEL_SOURCES = ("mfma_attn.hip", "common.h", "launch.h")
+KERNEL_SOURCES = ("mfma_attn.hip", "common.h")
+ARGS_DECL = ("launch.h", "struct AttnArgs {")
 
 
 def kernel_source_hash() -> str:
@@ -62,4 +64,9 @@ def kernel_source_hash() -> str:
     for name in KERNEL_SOURCES:
         with open(os.path.join(_CSRC, name), "rb") as fh:
             h.update(fh.read())
+    name, start = ARGS_DECL
+    with open(os.path.join(_CSRC, name)) as fh:
+        text = fh.read()
+    i = text.index(start)
+    h.update(text[i: text.index("};", i) + 2].encode())
     return h.hexdigest()
