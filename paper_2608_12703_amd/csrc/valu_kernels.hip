@@ -32,50 +32,54 @@ struct VStage<BF16> {
   uint4 w;
 };
 
+// Every load is issued unconditionally (rows and columns past the matrix read its last
+// row or column, steps past K its last step), so the number of loads in flight is the
+// same on every path and the compiler's waits count exactly; the values outside the
+// matrix become zeros when the step is staged in LDS.
 template <class S>
 __device__ __forceinline__ void vstage_load(VStage<S>& st, int kb, int M, int N, int K, const float* A,
                                             const typename S::T* W, int m0, int n0, int tid) {
-  const int k0 = kb * 32;
-  const bool kin = k0 < K;
+  const int k0 = min(kb * 32, K - 32);
   const int ar = tid >> 3, ak = (tid & 7) * 4;
-  const int m = m0 + ar;
-  st.a = (kin && m < M) ? *(const float4*)(A + (size_t)m * K + k0 + ak) : float4{0.f, 0.f, 0.f, 0.f};
+  st.a = *(const float4*)(A + (size_t)min(m0 + ar, M - 1) * K + k0 + ak);
   if constexpr (sizeof(typename S::T) == 4) {
     const int wr = tid >> 3, wk = (tid & 7) * 4;
-    const int n1 = n0 + wr, n2 = n0 + wr + 32;
-    st.w0 = (kin && n1 < N) ? *(const float4*)(W + (size_t)n1 * K + k0 + wk) : float4{0.f, 0.f, 0.f, 0.f};
-    st.w1 = (kin && n2 < N) ? *(const float4*)(W + (size_t)n2 * K + k0 + wk) : float4{0.f, 0.f, 0.f, 0.f};
+    st.w0 = *(const float4*)(W + (size_t)min(n0 + wr, N - 1) * K + k0 + wk);
+    st.w1 = *(const float4*)(W + (size_t)min(n0 + wr + 32, N - 1) * K + k0 + wk);
   } else {
     const int wb = tid >> 2, wk = (tid & 3) * 8;
-    const int n = n0 + wb;
-    st.w = (kin && n < N) ? *(const uint4*)(W + (size_t)n * K + k0 + wk) : make_uint4(0, 0, 0, 0);
+    st.w = *(const uint4*)(W + (size_t)min(n0 + wb, N - 1) * K + k0 + wk);
   }
 }
 
 template <class S>
-__device__ __forceinline__ void vstage_put(const VStage<S>& st, float (*As)[33], float (*Ws)[33], int tid) {
+__device__ __forceinline__ void vstage_put(const VStage<S>& st, int M, int N, int m0, int n0,
+                                           float (*As)[33], float (*Ws)[33], int tid) {
   const int ar = tid >> 3, ak = (tid & 7) * 4;
-  As[ar][ak + 0] = st.a.x;
-  As[ar][ak + 1] = st.a.y;
-  As[ar][ak + 2] = st.a.z;
-  As[ar][ak + 3] = st.a.w;
+  const bool am = m0 + ar < M;
+  As[ar][ak + 0] = am ? st.a.x : 0.f;
+  As[ar][ak + 1] = am ? st.a.y : 0.f;
+  As[ar][ak + 2] = am ? st.a.z : 0.f;
+  As[ar][ak + 3] = am ? st.a.w : 0.f;
   if constexpr (sizeof(typename S::T) == 4) {
     const int wr = tid >> 3, wk = (tid & 7) * 4;
-    Ws[wr][wk + 0] = st.w0.x;
-    Ws[wr][wk + 1] = st.w0.y;
-    Ws[wr][wk + 2] = st.w0.z;
-    Ws[wr][wk + 3] = st.w0.w;
-    Ws[wr + 32][wk + 0] = st.w1.x;
-    Ws[wr + 32][wk + 1] = st.w1.y;
-    Ws[wr + 32][wk + 2] = st.w1.z;
-    Ws[wr + 32][wk + 3] = st.w1.w;
+    const bool w0 = n0 + wr < N, w1 = n0 + wr + 32 < N;
+    Ws[wr][wk + 0] = w0 ? st.w0.x : 0.f;
+    Ws[wr][wk + 1] = w0 ? st.w0.y : 0.f;
+    Ws[wr][wk + 2] = w0 ? st.w0.z : 0.f;
+    Ws[wr][wk + 3] = w0 ? st.w0.w : 0.f;
+    Ws[wr + 32][wk + 0] = w1 ? st.w1.x : 0.f;
+    Ws[wr + 32][wk + 1] = w1 ? st.w1.y : 0.f;
+    Ws[wr + 32][wk + 2] = w1 ? st.w1.z : 0.f;
+    Ws[wr + 32][wk + 3] = w1 ? st.w1.w : 0.f;
   } else {
     const int wb = tid >> 2, wk = (tid & 3) * 8;
+    const bool wn = n0 + wb < N;
     const uint32_t u[4] = {st.w.x, st.w.y, st.w.z, st.w.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      Ws[wb][wk + 2 * j] = bf16_to_f32(u[j] & 0xffff);
-      Ws[wb][wk + 2 * j + 1] = bf16_to_f32(u[j] >> 16);
+      Ws[wb][wk + 2 * j] = wn ? bf16_to_f32(u[j] & 0xffff) : 0.f;
+      Ws[wb][wk + 2 * j + 1] = wn ? bf16_to_f32(u[j] >> 16) : 0.f;
     }
   }
 }
@@ -105,13 +109,15 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
   // step kb: stage its operands in LDS, multiply, request step kb + kVStages into the
   // freed registers
 #define VGEMM_STEP(ST, J)                                                 \
-  if (kb + (J) < KB) {                                                    \
-    __syncthreads();                                                      \
-    vstage_put<S>(ST, As, Ws, tid);                                       \
-    __syncthreads();                                                      \
-    _Pragma("unroll 8") for (int kk = 0; kk < 32; ++kk) {                 \
-      const float w = Ws[tx][kk];                                         \
-      _Pragma("unroll") for (int r = 0; r < 8; ++r) acc[r] = fmaf(As[ty * 8 + r][kk], w, acc[r]); \
+  {                                                                       \
+    if (kb + (J) < KB) {                                                  \
+      __syncthreads();                                                    \
+      vstage_put<S>(ST, M, N, m0, n0, As, Ws, tid);                       \
+      __syncthreads();                                                    \
+      _Pragma("unroll 8") for (int kk = 0; kk < 32; ++kk) {               \
+        const float w = Ws[tx][kk];                                       \
+        _Pragma("unroll") for (int r = 0; r < 8; ++r) acc[r] = fmaf(As[ty * 8 + r][kk], w, acc[r]); \
+      }                                                                   \
     }                                                                     \
     vstage_load<S>(ST, kb + (J) + kVStages, M, N, K, A, W, m0, n0, tid);  \
   }
@@ -207,43 +213,42 @@ struct AStage<BF16> {
 
 // Load chunk c0 (keys c0 .. c0 + 63): piece u of this thread is key run (key tid / 8 +
 // 32 u, lanes 8 (tid % 8) ..) and value run (lane tid / 8 + 32 u, keys c0 + 8 (tid % 8) ..).
-// Keys at or past n_keys read as zeros; a chunk at or past n_keys issues no loads.
+// Keys at or past n_keys read the last key's place (the values become zeros in LDS).
 template <class S, bool CROSS>
 __device__ __forceinline__ void astage_load(AStage<S>& st, int c0, int n_keys, int layer, int h, int H,
                                             int b, const SeqDesc& s, const typename S::T* kv,
                                             int num_pages, const int* block_table, int pages_per_seq,
                                             int frames_cap, int tid) {
   constexpr bool F = sizeof(typename S::T) == 4;
+  const int last = max(n_keys - 1, 0);
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int tk = c0 + (tid >> 3) + 32 * u, jk = (tid & 7) * 8;   // key run
     const int jv = (tid >> 3) + 32 * u, tv = c0 + (tid & 7) * 8;   // value run
     size_t bk = 0, bv = 0;
     if (CROSS) {
-      bk = cross_base(layer, h, H, frames_cap) + cross_off(0, s.enc_off + min(tk, n_keys - 1), jk);
-      bv = cross_base(layer, h, H, frames_cap) + cross_off(1, s.enc_off + min(tv, n_keys - 1) / 8 * 8, jv);
+      bk = cross_base(layer, h, H, frames_cap) + cross_off(0, s.enc_off + min(tk, last), jk);
+      bv = cross_base(layer, h, H, frames_cap) + cross_off(1, s.enc_off + min(tv, last) / 8 * 8, jv);
     } else {
-      const int pk = min(max(block_table[(size_t)b * pages_per_seq + min(tk, n_keys - 1) / kTile], 0), num_pages - 1);
-      const int pv = min(max(block_table[(size_t)b * pages_per_seq + min(tv, n_keys - 1) / kTile], 0), num_pages - 1);
-      bk = kv_tile_base(layer, 0, pk, h, num_pages, H) + tile_off(0, min(tk, n_keys - 1) % kTile, jk);
-      bv = kv_tile_base(layer, 1, pv, h, num_pages, H) + tile_off(1, min(tv, n_keys - 1) / 8 * 8 % kTile, jv);
+      const int pk = min(max(block_table[(size_t)b * pages_per_seq + min(tk, last) / kTile], 0), num_pages - 1);
+      const int pv = min(max(block_table[(size_t)b * pages_per_seq + min(tv, last) / kTile], 0), num_pages - 1);
+      bk = kv_tile_base(layer, 0, pk, h, num_pages, H) + tile_off(0, min(tk, last) % kTile, jk);
+      bv = kv_tile_base(layer, 1, pv, h, num_pages, H) + tile_off(1, min(tv, last) / 8 * 8 % kTile, jv);
     }
-    const bool kin = tk < n_keys, vin = tv < n_keys;
     if constexpr (F) {
-      const float4 z{0.f, 0.f, 0.f, 0.f};
-      st.k[u][0] = kin ? *(const float4*)(kv + bk) : z;
-      st.k[u][1] = kin ? *(const float4*)(kv + bk + 4) : z;
-      st.v[u][0] = vin ? *(const float4*)(kv + bv) : z;
-      st.v[u][1] = vin ? *(const float4*)(kv + bv + 4) : z;
+      st.k[u][0] = *(const float4*)(kv + bk);
+      st.k[u][1] = *(const float4*)(kv + bk + 4);
+      st.v[u][0] = *(const float4*)(kv + bv);
+      st.v[u][1] = *(const float4*)(kv + bv + 4);
     } else {
-      st.k[u] = kin ? *(const uint4*)(kv + bk) : make_uint4(0, 0, 0, 0);
-      st.v[u] = vin ? *(const uint4*)(kv + bv) : make_uint4(0, 0, 0, 0);
+      st.k[u] = *(const uint4*)(kv + bk);
+      st.v[u] = *(const uint4*)(kv + bv);
     }
   }
 }
 
-// Chunk c0's registers into LDS: ks[key][lane], vs[key][lane]; value slots at or past
-// n_keys are zeroed.
+// Chunk c0's registers into LDS: ks[key][lane], vs[key][lane]; key and value slots at
+// or past n_keys are zeroed.
 template <class S>
 __device__ __forceinline__ void astage_put(const AStage<S>& st, int c0, int n_keys, float (*ks)[65],
                                            float (*vs)[65], int tid) {
@@ -268,9 +273,10 @@ __device__ __forceinline__ void astage_put(const AStage<S>& st, int c0, int n_ke
         vx[2 * j + 1] = bf16_to_f32(vu[j] >> 16);
       }
     }
+    const bool kin = c0 + rk < n_keys;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      ks[rk][jk + e] = kx[e];
+      ks[rk][jk + e] = kin ? kx[e] : 0.f;
       vs[rv + e][jv] = (c0 + rv + e < n_keys) ? vx[e] : 0.f;
     }
   }
@@ -307,10 +313,10 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
     float m_run = -INFINITY, l_run = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
     const int c_first = lo / 64 * 64, nch = n_keys > c_first ? (n_keys - c_first + 63) / 64 : 0;
     AStage<S> st0, st1, st2, st3;
+    // (chunks past the last one reread it; nch >= 1 whenever the loop runs)
     auto load = [&](AStage<S>& st, int ci) {
-      if (ci < nch)
-        astage_load<S, CROSS>(st, c_first + ci * 64, n_keys, layer, h, H, b, s, kv, num_pages, block_table,
-                              pages_per_seq, frames_cap, tid);
+      astage_load<S, CROSS>(st, c_first + min(ci, max(nch - 1, 0)) * 64, n_keys, layer, h, H, b, s, kv,
+                            num_pages, block_table, pages_per_seq, frames_cap, tid);
     };
     load(st0, 0);
     load(st1, 1);
@@ -358,13 +364,15 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
     // chunk ci of the ring slot ST: stage it in LDS, request chunk ci + kAStages into the
     // freed registers, attend
 #define VATT_CHUNK(ST, J)                                  \
-  if (ci + (J) < nch) {                                    \
-    const int c0 = c_first + (ci + (J)) * 64;              \
-    __syncthreads();                                       \
-    astage_put<S>(ST, c0, n_keys, ks, vs, tid);            \
+  {                                                        \
+    if (ci + (J) < nch) {                                  \
+      const int c0 = c_first + (ci + (J)) * 64;            \
+      __syncthreads();                                     \
+      astage_put<S>(ST, c0, n_keys, ks, vs, tid);          \
+      __syncthreads();                                     \
+      attend(c0);                                          \
+    }                                                      \
     load(ST, ci + (J) + kAStages);                         \
-    __syncthreads();                                       \
-    attend(c0);                                            \
   }
     for (int ci = 0; ci < nch; ci += kAStages) {
       VATT_CHUNK(st0, 0)
