@@ -84,6 +84,8 @@ struct Workspace {
   float* q;        // queries [M][d]
   float* att;      // float32 path: attention output [M][d]
   float* hid;      // float32 path: GELU output [M][F]
+  float* apart;    // float32 path: attention partials per key group
+  int gself, gcross;   // float32 path: key groups of self- and cross-attention
   float* hidden;   // final LayerNorm output [M][d]
   float* logits;   // float32 path: [M][V]
   int* greedy;     // [M]
@@ -125,6 +127,9 @@ Workspace carve(const ad_model_desc& d, int M, int B, int k_max, char* base) {
     w.ln = (float*)take(4 * M * D);
     w.att = (float*)take(4 * M * D);
     w.hid = (float*)take(4 * M * F);
+    w.gself = ad::attn_valu_groups(d.max_pos);
+    w.gcross = ad::attn_valu_groups(d.max_frames);
+    w.apart = (float*)take(4 * ad::attn_valu_part_floats(M, d.n_heads, std::max(w.gself, w.gcross)));
     w.logits = (float*)take(4 * M * V);
   } else {
     const int Mp = w.RT * 16;
@@ -245,9 +250,9 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     ad::launch_gemm_valu<S>(ad::EPI_QKV, M, 3 * d, d, w.ln, lp(m, l, W_QKV), lp(m, l, B_QKV), e, st);
     {
       ProfScope ps(m, AD_PROF_SELF_ATTN, st);
-      ad::launch_self_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->kv.pool,
-                                   s->kv.num_pages, s->kv.block_table, s->kv.pages_per_seq, w.tree,
-                                   st);
+      ad::launch_self_attn_valu<S>(s->batch, M, H, d, l, w.seqs, w.rows, w.q, w.apart, w.gself, w.att,
+                                   s->kv.pool, s->kv.num_pages, s->kv.block_table, s->kv.pages_per_seq,
+                                   w.tree, st);
     }
     e.out = w.x; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, d, w.att, lp(m, l, W_O), lp(m, l, B_O), e, st);
@@ -262,8 +267,8 @@ void run_step_valu(const ad_model* m, const ad_step* s, const Workspace& w, hipS
     }
     {
       ProfScope ps(m, AD_PROF_CROSS_ATTN, st);
-      ad::launch_cross_attn_valu<S>(s->batch, H, d, l, w.seqs, w.q, w.att, s->cross.data,
-                                    s->cross.frames_cap, st);
+      ad::launch_cross_attn_valu<S>(s->batch, M, H, d, l, w.seqs, w.rows, w.q, w.apart, w.gcross, w.att,
+                                    s->cross.data, s->cross.frames_cap, st);
     }
     e.out = w.x; e.ldo = d;
     ad::launch_gemm_valu<S>(ad::EPI_RESID, M, d, d, w.att, lp(m, l, W_XO), lp(m, l, B_XO), e, st);

@@ -260,13 +260,18 @@ void launch_sum_partials_bias(int M, int N, int nsplit, const float* P, const vo
                               hipStream_t st);
 
 // Attention of every block row over the paged self cache (causal inside the block) or
-// over the sequence's encoder frames.  q and out are float32 [rows][d].
+// over the sequence's encoder frames.  q and out are float32 [rows][d]; part is scratch
+// of attn_valu_part_floats(M, H, G) floats, G = attn_valu_groups(the longest key range:
+// max_pos for self-attention, max_frames for cross-attention).
+int attn_valu_groups(int max_keys);
+inline size_t attn_valu_part_floats(int M, int H, int G) { return (size_t)M * H * G * (2 + 64); }
 template <class S>
-void launch_self_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
-                           float* out, const void* pool, int num_pages, const int* block_table,
-                           int pages_per_seq, const RowTree* tree, hipStream_t st);
+void launch_self_attn_valu(int B, int M, int H, int d, int layer, const SeqDesc* seqs, const RowDesc* rows,
+                           const float* q, float* part, int G, float* out, const void* pool, int num_pages,
+                           const int* block_table, int pages_per_seq, const RowTree* tree, hipStream_t st);
 template <class S>
-void launch_cross_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
-                            float* out, const void* cross, int frames_cap, hipStream_t st);
+void launch_cross_attn_valu(int B, int M, int H, int d, int layer, const SeqDesc* seqs, const RowDesc* rows,
+                            const float* q, float* part, int G, float* out, const void* cross, int frames_cap,
+                            hipStream_t st);
 
 }  // namespace ad

@@ -191,14 +191,18 @@ template void launch_gemm_valu<F32>(int, int, int, int, const float*, const void
 template void launch_gemm_valu<BF16>(int, int, int, int, const float*, const void*, const void*, const EpiArgs&, hipStream_t);
 
 // ---------------------------------------------------------------- attention
-// One block per (head, sequence).  Queries are taken 16 at a time; keys stream through
-// LDS in chunks of 64 at absolute positions 0, 64, 128, ... with an online softmax per
-// query.  A key a query may not see contributes exp(-inf) = 0; keys past every query's
+// One block per (head, sequence, group of kVGroupKeys keys at absolute positions 0, 128,
+// 256, ...).  Queries are taken 16 at a time; a group's keys stream through LDS in
+// chunks of 64 with an online softmax per query, which leaves a partial (max, sum,
+// unnormalised output) per (row, head, group); a second kernel merges the groups in
+// group order.  A key a query may not see contributes exp(-inf) = 0; keys past every query's
 // range are staged as zeros so stale cache slots never reach the output.  Every thread
 // requests its part of a chunk (two runs of 8 keys' lanes and two runs of 8 values of
 // one lane, contiguous in both cache layouts) kAStages chunks ahead into registers.
 
 constexpr int kAStages = 4;
+constexpr int kVGroupKeys = 128;   // keys per workgroup
+constexpr int kVPart = 2 + kHead;  // a partial: max, sum, 64 output lanes
 
 template <class S>
 struct AStage;
@@ -285,7 +289,7 @@ __device__ __forceinline__ void astage_put(const AStage<S>& st, int c0, int n_ke
 template <class S, bool CROSS>
 __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
                                                         const SeqDesc* seqs, const float* q,
-                                                        float* out, const typename S::T* kv,
+                                                        float* apart, int G, const typename S::T* kv,
                                                         int num_pages, const int* block_table,
                                                         int pages_per_seq, int frames_cap,
                                                         const RowTree* tree) {
@@ -293,7 +297,7 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
   __shared__ float ks[64][65];
   __shared__ float vs[64][65];
   __shared__ float ps[16][65];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y, g = blockIdx.z, tid = threadIdx.x;
   const SeqDesc s = seqs[b];
   if (!s.valid) return;
   const int qi = tid >> 4, part = tid & 15;
@@ -311,7 +315,10 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
     const unsigned long long tm = (!CROSS && qi < nq) ? tree[s.row0 + qg + qi].mask : 0ull;
     const int n_keys = CROSS ? s.whi : s.n + qg + nq;
     float m_run = -INFINITY, l_run = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
-    const int c_first = lo / 64 * 64, nch = n_keys > c_first ? (n_keys - c_first + 63) / 64 : 0;
+    // this group's chunks: keys [max(lo, 128 g), min(128 (g + 1), n_keys)), 64-aligned
+    const int c_first = max(lo / 64 * 64, g * kVGroupKeys);
+    const int c_end = min((g + 1) * kVGroupKeys, n_keys);
+    const int nch = c_end > c_first ? (c_end - c_first + 63) / 64 : 0;
     AStage<S> st0, st1, st2, st3;
     // (chunks past the last one reread it; nch >= 1 whenever the loop runs)
     auto load = [&](AStage<S>& st, int ci) {
@@ -381,30 +388,62 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
       VATT_CHUNK(st3, 3)
     }
 #undef VATT_CHUNK
+    // the group's partial: (max, sum, unnormalised output); a group without keys leaves
+    // (-inf, 0, 0)
     if (qi < nq) {
+      float* pp = apart + (((size_t)(s.row0 + qg + qi) * H + h) * G + g) * kVPart;
+      if (part == 0) {   // one of the row's 16 threads writes the statistics
+        pp[0] = m_run;
+        pp[1] = l_run;
+      }
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        out[(size_t)(s.row0 + qg + qi) * d + h * kHead + part * 4 + r] = o[r] / l_run;
+      for (int r = 0; r < 4; ++r) pp[2 + part * 4 + r] = o[r];
     }
   }
 }
 
+// Merge the G key groups of every (row, head) in group order: out = sum_g e^(m_g - M)
+// o_g / sum_g e^(m_g - M) l_g with M = max_g m_g.  Rows of no sequence, or of a sequence
+// the step skips, are left alone (as the attention kernel leaves them).
+__global__ void __launch_bounds__(64) attn_merge_kernel(int H, int d, int G, const SeqDesc* seqs,
+                                                        const RowDesc* rows, const float* part, float* out) {
+  const int m = blockIdx.x, h = blockIdx.y, j = threadIdx.x;
+  const int sq = rows[m].seq;
+  if (sq < 0 || !seqs[sq].valid) return;
+  const float* pp = part + ((size_t)m * H + h) * G * kVPart;
+  float M = -INFINITY;
+  for (int g = 0; g < G; ++g) M = fmaxf(M, pp[g * kVPart]);
+  float L = 0.f, acc = 0.f;
+  for (int g = 0; g < G; ++g) {
+    const float mg = pp[g * kVPart];
+    const float w = mg == -INFINITY ? 0.f : expf(mg - M);
+    L += w * pp[g * kVPart + 1];
+    acc += w * pp[g * kVPart + 2 + j];
+  }
+  out[(size_t)m * d + h * kHead + j] = acc / L;
+}
+
+int attn_valu_groups(int max_keys) { return (max_keys + kVGroupKeys - 1) / kVGroupKeys; }
+
 template <class S>
-void launch_self_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
-                           float* out, const void* pool, int num_pages, const int* block_table,
-                           int pages_per_seq, const RowTree* tree, hipStream_t st) {
-  hipLaunchKernelGGL((attn_valu_kernel<S, false>), dim3(H, B), dim3(256), 0, st, H, d, layer, seqs, q, out,
-                     (const typename S::T*)pool, num_pages, block_table, pages_per_seq, 0, tree);
+void launch_self_attn_valu(int B, int M, int H, int d, int layer, const SeqDesc* seqs, const RowDesc* rows,
+                           const float* q, float* part, int G, float* out, const void* pool, int num_pages,
+                           const int* block_table, int pages_per_seq, const RowTree* tree, hipStream_t st) {
+  hipLaunchKernelGGL((attn_valu_kernel<S, false>), dim3(H, B, G), dim3(256), 0, st, H, d, layer, seqs, q, part,
+                     G, (const typename S::T*)pool, num_pages, block_table, pages_per_seq, 0, tree);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(M, H), dim3(64), 0, st, H, d, G, seqs, rows, part, out);
 }
 template <class S>
-void launch_cross_attn_valu(int B, int H, int d, int layer, const SeqDesc* seqs, const float* q,
-                            float* out, const void* cross, int frames_cap, hipStream_t st) {
-  hipLaunchKernelGGL((attn_valu_kernel<S, true>), dim3(H, B), dim3(256), 0, st, H, d, layer, seqs, q, out,
-                     (const typename S::T*)cross, 0, nullptr, 0, frames_cap, nullptr);
+void launch_cross_attn_valu(int B, int M, int H, int d, int layer, const SeqDesc* seqs, const RowDesc* rows,
+                            const float* q, float* part, int G, float* out, const void* cross, int frames_cap,
+                            hipStream_t st) {
+  hipLaunchKernelGGL((attn_valu_kernel<S, true>), dim3(H, B, G), dim3(256), 0, st, H, d, layer, seqs, q, part,
+                     G, (const typename S::T*)cross, 0, nullptr, 0, frames_cap, nullptr);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(M, H), dim3(64), 0, st, H, d, G, seqs, rows, part, out);
 }
-template void launch_self_attn_valu<F32>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
-template void launch_self_attn_valu<BF16>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
-template void launch_cross_attn_valu<F32>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, hipStream_t);
-template void launch_cross_attn_valu<BF16>(int, int, int, int, const SeqDesc*, const float*, float*, const void*, int, hipStream_t);
+template void launch_self_attn_valu<F32>(int, int, int, int, int, const SeqDesc*, const RowDesc*, const float*, float*, int, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
+template void launch_self_attn_valu<BF16>(int, int, int, int, int, const SeqDesc*, const RowDesc*, const float*, float*, int, float*, const void*, int, const int*, int, const RowTree*, hipStream_t);
+template void launch_cross_attn_valu<F32>(int, int, int, int, int, const SeqDesc*, const RowDesc*, const float*, float*, int, float*, const void*, int, hipStream_t);
+template void launch_cross_attn_valu<BF16>(int, int, int, int, int, const SeqDesc*, const RowDesc*, const float*, float*, int, float*, const void*, int, hipStream_t);
 
 }  // namespace ad
