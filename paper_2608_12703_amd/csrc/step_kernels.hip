@@ -346,12 +346,22 @@ __global__ void __launch_bounds__(256) argmax_kernel(int V, const float* logits,
   __syncthreads();
   Top2 t{-INFINITY, 0x7fffffff, -INFINITY};
   int bad = 0;
-  for (int j = threadIdx.x; j < V; j += 256) {
-    const float v = lr[j];
-    if (!isfinite(v)) { bad = 1; continue; }
+  // this thread's indices j = tid, tid + 256, ... in increasing order; sixteen loads are
+  // requested before they are used (a row's scan is otherwise one round trip per value)
+  auto take = [&](float v, int j) {
+    if (!isfinite(v)) { bad = 1; return; }
     if (v > t.v1) { t.v2 = t.v1; t.v1 = v; t.i1 = j; }
     else if (v > t.v2) { t.v2 = v; }
+  };
+  int j0 = threadIdx.x;
+  for (; j0 + 15 * 256 < V; j0 += 16 * 256) {
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = lr[j0 + u * 256];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) take(v[u], j0 + u * 256);
   }
+  for (int j = j0; j < V; j += 256) take(lr[j], j);
   if (bad) atomicOr(&bad_s, 1);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {

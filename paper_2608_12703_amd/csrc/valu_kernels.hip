@@ -18,6 +18,15 @@ namespace ad {
 
 constexpr int kVStages = 8;
 
+// Workgroup barrier for LDS traffic only: this wave's LDS operations complete, its global
+// loads stay in flight (__syncthreads would also wait for every outstanding load, which
+// empties the prefetch rings below at every step).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt 0; vmcnt and expcnt not waited for
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // One thread's slice of a K step: 4 activations of row ar; 8 weights (4 of rows wr and
 // wr + 32 in float32, or 8 of row wb in bf16).
 template <class S>
@@ -52,35 +61,37 @@ __device__ __forceinline__ void vstage_load(VStage<S>& st, int kb, int M, int N,
   }
 }
 
+// LDS layout of a step: activations transposed, At[k][row] (a row's 8 values of one k
+// are one broadcast read pair), weights Ws[col][k]; rows of 36 floats keep every
+// 16-byte read aligned and the weight reads of 16 lanes on distinct banks.
+constexpr int kVLd = 36;
+
 template <class S>
 __device__ __forceinline__ void vstage_put(const VStage<S>& st, int M, int N, int m0, int n0,
-                                           float (*As)[33], float (*Ws)[33], int tid) {
+                                           float (*At)[kVLd], float (*Ws)[kVLd], int tid) {
   const int ar = tid >> 3, ak = (tid & 7) * 4;
   const bool am = m0 + ar < M;
-  As[ar][ak + 0] = am ? st.a.x : 0.f;
-  As[ar][ak + 1] = am ? st.a.y : 0.f;
-  As[ar][ak + 2] = am ? st.a.z : 0.f;
-  As[ar][ak + 3] = am ? st.a.w : 0.f;
+  At[ak + 0][ar] = am ? st.a.x : 0.f;
+  At[ak + 1][ar] = am ? st.a.y : 0.f;
+  At[ak + 2][ar] = am ? st.a.z : 0.f;
+  At[ak + 3][ar] = am ? st.a.w : 0.f;
   if constexpr (sizeof(typename S::T) == 4) {
     const int wr = tid >> 3, wk = (tid & 7) * 4;
     const bool w0 = n0 + wr < N, w1 = n0 + wr + 32 < N;
-    Ws[wr][wk + 0] = w0 ? st.w0.x : 0.f;
-    Ws[wr][wk + 1] = w0 ? st.w0.y : 0.f;
-    Ws[wr][wk + 2] = w0 ? st.w0.z : 0.f;
-    Ws[wr][wk + 3] = w0 ? st.w0.w : 0.f;
-    Ws[wr + 32][wk + 0] = w1 ? st.w1.x : 0.f;
-    Ws[wr + 32][wk + 1] = w1 ? st.w1.y : 0.f;
-    Ws[wr + 32][wk + 2] = w1 ? st.w1.z : 0.f;
-    Ws[wr + 32][wk + 3] = w1 ? st.w1.w : 0.f;
+    *(float4*)&Ws[wr][wk] = w0 ? st.w0 : float4{0.f, 0.f, 0.f, 0.f};
+    *(float4*)&Ws[wr + 32][wk] = w1 ? st.w1 : float4{0.f, 0.f, 0.f, 0.f};
   } else {
     const int wb = tid >> 2, wk = (tid & 3) * 8;
     const bool wn = n0 + wb < N;
     const uint32_t u[4] = {st.w.x, st.w.y, st.w.z, st.w.w};
+    float f[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      Ws[wb][wk + 2 * j] = wn ? bf16_to_f32(u[j] & 0xffff) : 0.f;
-      Ws[wb][wk + 2 * j + 1] = wn ? bf16_to_f32(u[j] >> 16) : 0.f;
+      f[2 * j] = wn ? bf16_to_f32(u[j] & 0xffff) : 0.f;
+      f[2 * j + 1] = wn ? bf16_to_f32(u[j] >> 16) : 0.f;
     }
+    *(float4*)&Ws[wb][wk] = float4{f[0], f[1], f[2], f[3]};
+    *(float4*)&Ws[wb][wk + 4] = float4{f[4], f[5], f[6], f[7]};
   }
 }
 
@@ -89,8 +100,8 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
                                                         const typename S::T* W,
                                                         const typename S::T* bias, EpiArgs e) {
   static_assert(sizeof(typename SA::T) == 4, "float32 activations");
-  __shared__ float As[32][33];
-  __shared__ float Ws[64][33];
+  __shared__ __align__(16) float At[32][kVLd];
+  __shared__ __align__(16) float Ws[64][kVLd];
   const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
   const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 64;
   const int KB = K / 32;
@@ -111,12 +122,18 @@ __global__ void __launch_bounds__(256) gemm_valu_kernel(int M, int N, int K, con
 #define VGEMM_STEP(ST, J)                                                 \
   {                                                                       \
     if (kb + (J) < KB) {                                                  \
-      __syncthreads();                                                    \
-      vstage_put<S>(ST, M, N, m0, n0, As, Ws, tid);                       \
-      __syncthreads();                                                    \
-      _Pragma("unroll 8") for (int kk = 0; kk < 32; ++kk) {               \
-        const float w = Ws[tx][kk];                                       \
-        _Pragma("unroll") for (int r = 0; r < 8; ++r) acc[r] = fmaf(As[ty * 8 + r][kk], w, acc[r]); \
+      lds_barrier();                                                      \
+      vstage_put<S>(ST, M, N, m0, n0, At, Ws, tid);                       \
+      lds_barrier();                                                      \
+      _Pragma("unroll") for (int k4 = 0; k4 < 32; k4 += 4) {              \
+        const float4 w = *(const float4*)&Ws[tx][k4];                     \
+        const float wv[4] = {w.x, w.y, w.z, w.w};                         \
+        _Pragma("unroll") for (int u = 0; u < 4; ++u) {                   \
+          const float4 a0 = *(const float4*)&At[k4 + u][ty * 8];          \
+          const float4 a1 = *(const float4*)&At[k4 + u][ty * 8 + 4];      \
+          const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w}; \
+          _Pragma("unroll") for (int r = 0; r < 8; ++r) acc[r] = fmaf(av[r], wv[u], acc[r]); \
+        }                                                                 \
       }                                                                   \
     }                                                                     \
     vstage_load<S>(ST, kb + (J) + kVStages, M, N, K, A, W, m0, n0, tid);  \
@@ -304,7 +321,7 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
   const int n_rows = s.k + 1;
   for (int qg = 0; qg < n_rows; qg += 16) {
     const int nq = min(16, n_rows - qg);
-    __syncthreads();
+    lds_barrier();
     for (int i = tid; i < 16 * 64; i += 256) {
       const int r = i >> 6, j = i & 63;
       qs[r][j] = r < nq ? q[(size_t)(s.row0 + qg + r) * d + h * kHead + j] : 0.f;
@@ -359,7 +376,7 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
       for (int off = 8; off >= 1; off >>= 1) ls += __shfl_xor(ls, off, kWave);
       l_run = l_run * scale + ls;
       m_run = m_new;
-      __syncthreads();
+      lds_barrier();
 #pragma unroll
       for (int r = 0; r < 4; ++r) o[r] *= scale;
       for (int key = 0; key < 64; ++key) {
@@ -374,9 +391,9 @@ __global__ void __launch_bounds__(256) attn_valu_kernel(int H, int d, int layer,
   {                                                        \
     if (ci + (J) < nch) {                                  \
       const int c0 = c_first + (ci + (J)) * 64;            \
-      __syncthreads();                                     \
+      lds_barrier();                                       \
       astage_put<S>(ST, c0, n_keys, ks, vs, tid);          \
-      __syncthreads();                                     \
+      lds_barrier();                                       \
       attend(c0);                                          \
     }                                                      \
     load(ST, ci + (J) + kAStages);                         \
