@@ -174,7 +174,7 @@ typedef struct {
   float* out_hidden;          /* device [rows][d] out (optional): LN_f output        */
   float* out_margin;          /* device [rows] out (optional): top-1 minus top-2     */
   int32_t* err_flag;          /* device [1]: AD_ERR_* bits are OR-ed in              */
-  void* workspace;            /* device scratch, >= ad_workspace_size() bytes        */
+  void* workspace;            /* device scratch, >= ad_workspace_size() bytes, 256-byte aligned */
   size_t workspace_bytes;
   /* Verification-attention anchor readout (optional; paper, section "Correction and
    * Cost", paragraph "Verification-Attention Correction", and appendix "Runtime
@@ -286,8 +286,10 @@ ad_status ad_verify_step_static(const ad_model* model, const ad_step* step, void
  * verification-attention anchor; T_b from enc_len), the draft block's cross_window.
  * W_fuse [d][4d], W_in [d][2d], b_fuse, b_in: device arrays of the target's dtype; the
  * token table is the target's.  Skipped sequences (accept_len < 0) get zero features.
- * Errors: AD_EINVAL (NULL argument, bad layout), AD_ERANGE (batch < 1, rows < batch,
- * token_stride < 1, half_window < 0), AD_ENOSPACE (workspace too small).
+ * workspace: device, >= ad_draft_input_workspace_size() bytes, 256-byte aligned.
+ * Errors: AD_EINVAL (NULL argument, bad layout, misaligned workspace), AD_ERANGE (batch
+ * < 1, rows < batch, token_stride < 1, half_window < 0), AD_ENOSPACE (workspace too
+ * small).
  */
 ad_status ad_draft_input_workspace_size(const ad_model* target, int32_t batch, size_t* bytes);
 ad_status ad_draft_input(const ad_model* target, const void* w_fuse, const void* b_fuse,
@@ -344,8 +346,10 @@ ad_status ad_kv_commit_tree(const ad_model* model, const ad_kv* kv, const int32_
  * out_dfeat [rows][d] = dL/dfeat.  A centre outside [-1, T_b) or a sequence with bad
  * frames sets AD_ERR_FRAMES, a target outside [-1, vocab) AD_ERR_TOKEN; those rows are
  * left out.  Sums run in a fixed order (repeatable results).
- * Errors: AD_EINVAL (NULL argument or a missing companion input), AD_ERANGE (sizes,
- * layer, sigma <= 0, lambda < 0), AD_ENOSPACE, AD_EUNSUPPORTED (float32 model).
+ * workspace: device, >= ad_anchordraft_loss_workspace_size() bytes, 256-byte aligned.
+ * Errors: AD_EINVAL (NULL argument, a missing companion input or a misaligned
+ * workspace), AD_ERANGE (sizes, layer, sigma <= 0, lambda < 0), AD_ENOSPACE,
+ * AD_EUNSUPPORTED (float32 model).
  */
 ad_status ad_anchordraft_loss_workspace_size(const ad_model* draft, int32_t batch,
                                              int32_t rows_per_seq, size_t* bytes);
@@ -366,7 +370,8 @@ ad_status ad_anchordraft_loss(const ad_model* draft, const ad_cross* cross, int3
  *   next_tokens[b][i] = d_i
  * heads_w is device [n_heads][vocab][d] of the model dtype.  hidden is the out_hidden
  * of the step ([rows][d] float32).  Sequences with accept_len < 0 get -1 everywhere.
- * Errors: AD_EINVAL, AD_ERANGE, AD_ENOSPACE.
+ * workspace: device, >= ad_draft_heads_workspace_size() bytes, 256-byte aligned.
+ * Errors: AD_EINVAL (NULL argument, misaligned workspace), AD_ERANGE, AD_ENOSPACE.
  */
 ad_status ad_draft_heads(const ad_model* model, const void* heads_w, int32_t n_heads,
                          const float* hidden, int32_t layout, int32_t k_max,

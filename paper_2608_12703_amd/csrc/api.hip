@@ -614,6 +614,7 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
       return fail(AD_ERANGE, "tap_layers must be -1 or layer indices");
     if (s->tap_layers[i] >= 0 && !s->out_taps) return fail(AD_EINVAL, "tap_layers need out_taps");
   }
+  if ((uintptr_t)s->workspace % 256) return fail(AD_EINVAL, "workspace must be 256-byte aligned");
   const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");
@@ -698,6 +699,7 @@ ad_status ad_draft_input(const ad_model* model, const void* w_fuse, const void* 
   const int d = D.d_model;
   size_t need = 0;
   ad_draft_input_workspace_size(model, batch, &need);
+  if ((uintptr_t)workspace % 256) return fail(AD_EINVAL, "workspace must be 256-byte aligned");
   if (workspace_bytes < need) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need) + " bytes");
   (void)hipGetLastError();
   hipStream_t st = (hipStream_t)stream;
@@ -818,6 +820,7 @@ ad_status ad_anchordraft_loss(const ad_model* draft, const ad_cross* cross, int3
   if (out_dlogits && !logits) return fail(AD_EINVAL, "out_dlogits needs logits");
   if (out_dfeat && !feat) return fail(AD_EINVAL, "out_dfeat needs feat");
   const LossWs w = loss_ws(D, batch, rows_per_seq);
+  if ((uintptr_t)workspace % 256) return fail(AD_EINVAL, "workspace must be 256-byte aligned");
   if (workspace_bytes < w.bytes) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(w.bytes) + " bytes");
   char* base = (char*)workspace;
   ad::LossArgs a{};
@@ -927,6 +930,7 @@ ad_status ad_draft_heads(const ad_model* model, const void* heads_w, int32_t n_h
   if (n_heads < 1 || batch < 1 || k_max < 0) return fail(AD_ERANGE, "sizes out of range");
   size_t need = 0;
   ad_draft_heads_workspace_size(model, n_heads, batch, &need);
+  if ((uintptr_t)workspace % 256) return fail(AD_EINVAL, "workspace must be 256-byte aligned");
   if (workspace_bytes < need) return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need) + " bytes");
   const ad_model_desc& D = model->desc;
   char* base = (char*)workspace;

@@ -160,6 +160,19 @@ __device__ __forceinline__ void afrag_store(uint16_t* base, int RT, int m, int k
   base[afrag_index(m, k, 0, RT)] = hi;
   base[afrag_index(m, k, 1, RT)] = lo;
 }
+// Four consecutive values v.x .. v.w at columns k .. k + 3 (k % 4 == 0) of row m: one
+// 8-byte store each for hi and lo (the four lie in one run of eight).
+__device__ __forceinline__ void afrag_store4(uint16_t* base, int RT, int m, int k, float4 v) {
+  uint16_t h[4], l[4];
+  split_hilo(v.x, h[0], l[0]);
+  split_hilo(v.y, h[1], l[1]);
+  split_hilo(v.z, h[2], l[2]);
+  split_hilo(v.w, h[3], l[3]);
+  *(uint2*)(base + afrag_index(m, k, 0, RT)) =
+      make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+  *(uint2*)(base + afrag_index(m, k, 1, RT)) =
+      make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
+}
 
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at lds_wave + 16 l
 // (lds_wave must be the same for the whole wave).

@@ -128,7 +128,8 @@ size_t gemm_part_floats(int M, int N, int K);
 int lm_records(int V);
 
 // Matrix-core attention over bf16 caches; output in A-fragment order.
-constexpr int kAttnPart = 16 + 16 + 64 * 16;   // per chunk: max, sum, O^T (64 x 16)
+constexpr int kAttnORow = 68;                  // floats per query row of a chunk's output
+constexpr int kAttnPart = 16 + 16 + 16 * kAttnORow;   // per chunk: max, sum, O [16][68]
 constexpr int kSelfChunk = 128;                // keys per wave, self-attention
 constexpr int kCrossChunk = 384;               // frames per wave, cross-attention
 constexpr int kMaxBlockRows = 64;              // bf16 path: rows (k + 1) per sequence

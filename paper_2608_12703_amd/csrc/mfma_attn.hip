@@ -475,32 +475,39 @@ attn_mfma_kernel(AttnArgs a) {
       Pc[c16] = m_run;
       Pc[16 + c16] = l_run;
     }
+    // O row c16 (query), dims 16 dt + 4 grp .. + 3: one 16-byte LDS write each
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) Pc[32 + (dt * 16 + grp * 4 + i) * 16 + c16] = o[dt][i];
+      *(float4*)(Pc + 32 + c16 * kAttnORow + dt * 16 + grp * 4) = float4{o[dt][0], o[dt][1], o[dt][2], o[dt][3]};
   }
   // LDS-only barrier (the cache writes need not have landed)
   __builtin_amdgcn_s_waitcnt(0xc07f);
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 
-  // merge the chunks in chunk order: output (query qq, dim dd) per thread
-  for (int idx = threadIdx.x; idx < 16 * 64; idx += blockDim.x) {
-    const int qq = idx & 15, dd = idx >> 4;
+  // merge the chunks in chunk order: four consecutive dims d4 .. d4 + 3 of query qq per
+  // thread (every output's sums run in the same order as one output per thread)
+  for (int idx = threadIdx.x; idx < 16 * 16; idx += blockDim.x) {
+    const int qq = idx & 15, d4 = (idx >> 4) * 4;
     if (qq >= nq) continue;
     float M = -INFINITY;
     for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, part[c * kAttnPart + qq]);
-    float L = 0.f, acc = 0.f;
+    float L = 0.f;
+    float4 acc{0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < n_chunks; ++c) {
       const float* Q = part + c * kAttnPart;
       const float mc = Q[qq];
       const float wgt = (mc == -INFINITY) ? 0.f : __expf(mc - M);
       L += wgt * Q[16 + qq];
-      acc += wgt * Q[32 + dd * 16 + qq];
+      const float4 ov = *(const float4*)(Q + 32 + qq * kAttnORow + d4);
+      acc.x += wgt * ov.x;
+      acc.y += wgt * ov.y;
+      acc.z += wgt * ov.z;
+      acc.w += wgt * ov.w;
     }
-    afrag_store(a.out, a.out_RT, s.row0 + q0 + qq, h * kHead + dd, acc / L);
-    if (SCORES && dd == 0) a.stat_out[(size_t)(s.row0 + q0 + qq) * a.H + h] = float2{M, L};
+    afrag_store4(a.out, a.out_RT, s.row0 + q0 + qq, h * kHead + d4,
+                 float4{acc.x / L, acc.y / L, acc.z / L, acc.w / L});
+    if (SCORES && d4 == 0) a.stat_out[(size_t)(s.row0 + q0 + qq) * a.H + h] = float2{M, L};
   }
 }
 

@@ -93,8 +93,16 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }
     asm volatile("" ::: "memory");                           \
   } while (0)
 
+// Product order of one accumulator tile: SW computes the transposed tile (weights as the
+// first operand), so a lane holds four consecutive columns of one row instead of four
+// rows of one column; each element's sum is the same.
+template <bool SW>
+__device__ __forceinline__ f32x4 mma_tile(bf16x8 a, bf16x8 w, f32x4 c) {
+  return SW ? mfma_bf16(w, a, c) : mfma_bf16(a, w, c);
+}
+
 // One 32-wide K step of a wave: RW row tiles (row group rg) x 4 column tiles (half ch).
-template <int RTC>
+template <int RTC, bool SW>
 __device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][4], const uint4* abuf,
                                          const uint4* wbuf, int rg, int ch, int lane) {
   constexpr int RW = RTC / 4;
@@ -108,8 +116,8 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[RTC / 4][4], const uint4* 
     const bf16x8 al = as_bf16x8(abuf[(rt * 2 + 1) * 64 + lane]);
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
-      acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
-      acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
+      acc[r][ct] = mma_tile<SW>(ah, b[ct], acc[r][ct]);
+      acc[r][ct] = mma_tile<SW>(al, b[ct], acc[r][ct]);
     }
   }
 }
@@ -122,7 +130,7 @@ struct AFrag {
 
 // One 32-wide K step with the activations from registers: RW row tiles x CT column
 // tiles (column group ch).
-template <int RW, int CT>
+template <int RW, int CT, bool SW>
 __device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RW][CT], const AFrag<RW>& a,
                                              const uint4* wbuf, int ch, int lane) {
   bf16x8 b[CT];
@@ -133,8 +141,8 @@ __device__ __forceinline__ void mma_step_reg(f32x4 (&acc)[RW][CT], const AFrag<R
     const bf16x8 ah = as_bf16x8(a.h[r]), al = as_bf16x8(a.l[r]);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
-      acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
+      acc[r][ct] = mma_tile<SW>(ah, b[ct], acc[r][ct]);
+      acc[r][ct] = mma_tile<SW>(al, b[ct], acc[r][ct]);
     }
   }
 }
@@ -149,6 +157,10 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   constexpr int RW = WIDE ? 1 : RTC / 4;  // row tiles per wave
   constexpr int CT = WIDE ? 8 : 4;        // 16-column tiles per wave
   constexpr int NA = RTC / 4;            // direct loads per wave for one activation stage
+  // the up-projection keeps transposed tiles (four consecutive columns of a row per lane:
+  // 8-byte hi / lo stores).  (Measured slower for the split-K partials: 16-byte
+  // non-temporal stores of 16 rows per instruction against 4-byte stores of 4 rows.)
+  constexpr bool kSw = EPI == EPI_GELU;
   // Activation ring: 3 stages (requested 2 steps ahead); weight ring: 6 stages (requested
   // 5 steps ahead, covering HBM latency).  Distinct LDS objects, so the compiler can tell
   // a read of one stage from the direct loads still filling another.  (Measured slower:
@@ -237,8 +249,8 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
       iw(NW0, kb + 4);                                            \
       la(NA1, kb + 5);                                            \
       iw(NW1, kb + 5);                                            \
-      mma_step_reg<RW, CT>(acc, CA0, CW0, ch, lane);                 \
-      if (kb + 1 < kb1) mma_step_reg<RW, CT>(acc, CA1, CW1, ch, lane);\
+      mma_step_reg<RW, CT, kSw>(acc, CA0, CW0, ch, lane);                 \
+      if (kb + 1 < kb1) mma_step_reg<RW, CT, kSw>(acc, CA1, CW1, ch, lane);\
       BARRIER_VMCNT(kWait2);                                      \
       kb += 2;                                                    \
     }
@@ -268,7 +280,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     {                                               \
       la(NXA, kb + 5);                              \
       iw(NXW, kb + 5);                              \
-      mma_step_reg<RW, CT>(acc, CA, CW, ch, lane);  \
+      mma_step_reg<RW, CT, kSw>(acc, CA, CW, ch, lane);  \
       BARRIER_VMCNT(kWait);                         \
       ++kb;                                         \
     }
@@ -305,7 +317,7 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   {                                            \
     ia(NXA, kb + 2);                           \
     iw(NXW, kb + 5);                           \
-    mma_step<RTC>(acc, CA, CW, rg, ch, lane);  \
+    mma_step<RTC, kSw>(acc, CA, CW, rg, ch, lane);  \
     BARRIER_VMCNT(kWait);                      \
     ++kb;                                      \
   }
@@ -327,9 +339,10 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   }
   BARRIER_VMCNT(0);
 
-  // row / column of accumulator element (r, ct, i) of this lane
-  const int row_base = (rt0 + rg * RW) * 16 + grp * 4;   // + r * 16 + i
-  const int col_base = n0 + ch * CT * 16 + c16;          // + ct * 16
+  // row / column of accumulator element (r, ct, i) of this lane: row_base + r * 16 + i,
+  // col_base + ct * 16; with transposed tiles row_base + r * 16, col_base + ct * 16 + i
+  const int row_base = (rt0 + rg * RW) * 16 + (kSw ? c16 : grp * 4);
+  const int col_base = n0 + ch * CT * 16 + (kSw ? grp * 4 : c16);
 
   // This kernel's LDS is also written by direct loads, so the compiler orders every LDS
   // access after outstanding global stores; epilogues therefore finish all their
@@ -382,25 +395,30 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
 
   if (EPI == EPI_GELU) {
     // FFN up-projection (unsplit): bias + GELU, stored straight from registers as the
-    // next product's A operand (hi/lo bf16 pair in A-fragment order)
-    float bv[CT];
+    // next product's A operand (hi/lo bf16 pair in A-fragment order; four consecutive
+    // columns of a row are one 8-byte store each for hi and lo)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      const int n = min(col_base + ct * 16, g.N - 1);
-      bv[ct] = bf16_to_f32(g.bias[n]);
-    }
+      const int n = col_base + ct * 16;
+      float bv[4];
 #pragma unroll
-    for (int r = 0; r < RW; ++r)
+      for (int i = 0; i < 4; ++i) bv[i] = bf16_to_f32(g.bias[min(n + i, g.N - 1)]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = row_base + r * 16 + i;
+      for (int r = 0; r < RW; ++r) {
+        const int m = row_base + r * 16;
         if (m >= g.M) continue;
+        const float4 y{gelu_erf(acc[r][ct][0] + bv[0]), gelu_erf(acc[r][ct][1] + bv[1]),
+                       gelu_erf(acc[r][ct][2] + bv[2]), gelu_erf(acc[r][ct][3] + bv[3])};
+        if (n + 3 < g.N) {
+          afrag_store4(g.e.frag, g.e.frag_RT, m, n, y);
+        } else {
+          const float yv[4] = {y.x, y.y, y.z, y.w};
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const int n = col_base + ct * 16;
-          if (n < g.N) afrag_store(g.e.frag, g.e.frag_RT, m, n, gelu_erf(acc[r][ct][i] + bv[ct]));
+          for (int i = 0; i < 4; ++i)
+            if (n + i < g.N) afrag_store(g.e.frag, g.e.frag_RT, m, n + i, yv[i]);
         }
       }
+    }
     return;
   }
 

@@ -222,7 +222,7 @@ __global__ void __launch_bounds__(512) xkv_mfma_kernel(int M, int N, int K, cons
 // row 16 rt + l % 16, columns 32 kb + 8 (l / 16) .. + 7.  Each thread moves one 16-byte
 // piece; consecutive threads read consecutive pieces of a row.
 __global__ void __launch_bounds__(256) pack_rows_kernel(const uint16_t* A, int M, int K, uint16_t* P) {
-  const int RT = M / 16, KB = K / 32;
+  const int RT = M / 16;
   const size_t pieces = (size_t)M * K / 8;
   for (size_t q = (size_t)blockIdx.x * 256 + threadIdx.x; q < pieces; q += (size_t)gridDim.x * 256) {
     const int m = (int)(q / (K / 8)), k8 = (int)(q % (K / 8));

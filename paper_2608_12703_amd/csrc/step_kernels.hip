@@ -220,20 +220,6 @@ __device__ __forceinline__ float4 ld_bf16x4(const uint16_t* p, int j) {
                 bf16_to_f32(u.y >> 16)};
 }
 
-// Columns j .. j + 3 (j % 4 == 0) of row m in A-fragment order: they share one 8-wide
-// run, so the hi and lo halves are one 8-byte store each.
-__device__ __forceinline__ void afrag_store4(uint16_t* base, int RT, int m, int j, float4 v) {
-  uint16_t h[4], l[4];
-  split_hilo(v.x, h[0], l[0]);
-  split_hilo(v.y, h[1], l[1]);
-  split_hilo(v.z, h[2], l[2]);
-  split_hilo(v.w, h[3], l[3]);
-  *(uint2*)(base + afrag_index(m, j, 0, RT)) =
-      uint2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
-  *(uint2*)(base + afrag_index(m, j, 1, RT)) =
-      uint2{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
-}
-
 // Row of workgroup `bid` for the row-per-workgroup kernels that write A-fragment
 // operands.  Workgroups are dealt round-robin over the 8 XCDs; this numbering puts the
 // 8 rows that share each 128-byte line of the output (rows 8a .. 8a + 7) on one XCD, so

@@ -123,7 +123,7 @@ def test_verify_step_rejects_before_enqueue(ad):
         h, ctypes.byref(o.get("cross", cr)), o.get("layer", 0), o.get("batch", 2), 5,
         o.get("xq", 0x1000), o.get("center", 0x1000), o.get("sigma", 5.0), o.get("lam", 0.1),
         o.get("logits", None), o.get("targets", None), o.get("feat", None), None, 0x1000,
-        None, o.get("dxq", None), None, None, 0x1000, 0x1000, o.get("ws", lw.value), None)
+        None, o.get("dxq", None), None, None, 0x1000, o.get("wsp", 0x1000), o.get("ws", lw.value), None)
     assert loss(center=None) == -1                                  # xq without centres
     assert loss(logits=0x1000) == -1                                # logits without targets
     assert loss(feat=0x1000, targets=0x1000) == -1                  # feat without feat_target
@@ -131,6 +131,7 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert loss(batch=0) == -2 and loss(layer=cfg.n_layers) == -2
     assert loss(sigma=0.0) == -2 and loss(lam=-1.0) == -2
     assert loss(ws=lw.value - 1) == -3
+    assert loss(wsp=0x1010) == -1                                   # misaligned workspace
     ws = ctypes.c_size_t()
     assert ad.LIB.ad_draft_input_workspace_size(h, 2, ctypes.byref(ws)) == 0
     assert ws.value >= 7 * cfg.d_model * 2 * 4
@@ -138,7 +139,7 @@ def test_verify_step_rejects_before_enqueue(ad):
         h, o.get("w_fuse", 0x1000), 0x1000, 0x1000, 0x1000, o.get("batch", 2), o.get("taps", 0x1000),
         0x1000, o.get("layout", ad.AD_PADDED), 3, None, 0x1000, o.get("rows", 8), None, 0x1000,
         o.get("stride", 4), 0x1000, o.get("anchor", None), 0x1000, o.get("half", 20), 0x1000,
-        0x1000, 0x1000, o.get("ws", ws.value), None)
+        0x1000, o.get("wsp", 0x1000), o.get("ws", ws.value), None)
     assert di(w_fuse=None) == -1
     assert di(layout=7) == -1
     assert di(layout=ad.AD_PACKED) == -1                            # packed without cu_rows
@@ -146,8 +147,11 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert di(batch=0) == -2 and di(stride=0) == -2 and di(rows=1) == -2
     assert di(anchor=0x1000, half=-1) == -2
     assert di(ws=ws.value - 1) == -3
+    assert di(wsp=0x1010) == -1                                     # misaligned workspace
     assert run(_step(ad, workspace_bytes=100)) == -3
     assert b"workspace" in ad.LIB.ad_last_error()
+    assert run(_step(ad, workspace=0x1010)) == -1                   # misaligned workspace
+    assert b"aligned" in ad.LIB.ad_last_error()
     assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1
     assert ad.LIB.ad_kv_commit(0x1000, 0x1000, 0, None) == -2
     kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
@@ -169,6 +173,8 @@ def test_verify_step_rejects_before_enqueue(ad):
                                  0x1000, ws.value - 1, None) == -3
     assert ad.LIB.ad_draft_heads(h, 0x1000, 0, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
                                  0x1000, ws.value, None) == -2
+    assert ad.LIB.ad_draft_heads(h, 0x1000, 4, 0x1000, 0, 4, None, 0x1000, 0x1000, 1, 0x1000,
+                                 0x1010, ws.value, None) == -1      # misaligned workspace
     ad.LIB.ad_model_destroy(h)
 
 
