@@ -195,7 +195,7 @@ typedef struct {
    * receives, for each tap_layers[i] >= 0, the residual stream after that layer at every
    * row (the four target representations the draft reads are these three and
    * out_hidden).                                                                     */
-  const float* in_rows;       /* device [rows][d_model] (optional)                   */
+  const float* in_rows;       /* device [rows][d_model] (optional), 16-byte aligned  */
   const int32_t* cross_window; /* device [B][2] (optional)                           */
   int32_t tap_layers[3];      /* layer indices, -1 for none                          */
   float* out_taps;            /* device [3][rows][d_model] out (optional)            */

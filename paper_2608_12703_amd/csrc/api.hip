@@ -615,6 +615,7 @@ ad_status ad_verify_step(const ad_model* model, const ad_step* s, void* stream) 
     if (s->tap_layers[i] >= 0 && !s->out_taps) return fail(AD_EINVAL, "tap_layers need out_taps");
   }
   if ((uintptr_t)s->workspace % 256) return fail(AD_EINVAL, "workspace must be 256-byte aligned");
+  if ((uintptr_t)s->in_rows % 16) return fail(AD_EINVAL, "in_rows must be 16-byte aligned");
   const Workspace need = carve(D, s->rows, s->batch, s->k_max, nullptr);
   if (s->workspace_bytes < need.bytes)
     return fail(AD_ENOSPACE, "workspace needs " + std::to_string(need.bytes) + " bytes");

@@ -268,37 +268,34 @@ __global__ void __launch_bounds__(1024) reduce_res_ln_kernel(int M, int d, int n
   }
 }
 
-// Embedding of the block rows fused with the first LayerNorm.
-template <class S>
-__global__ void __launch_bounds__(256) embed_ln_kernel(int M, int d, const RowDesc* rows,
-                                                       const typename S::T* tok_emb,
-                                                       const typename S::T* pos_emb, float* x,
-                                                       const float* in_rows,
-                                                       const typename S::T* g,
-                                                       const typename S::T* b, uint16_t* frag,
-                                                       int RT) {
-  extern __shared__ float row[];
-  __shared__ float red[4];
-  const int m = xcd_row(blockIdx.x);
+// Embedding of the block rows fused with the first LayerNorm: x = E_tok[token] (or the
+// caller's input row) + E_pos[pos], then LN(x) * g + b in A-fragment order.  One thread
+// per 4 columns (blockDim = d / 4 rounded up to whole waves), every load up front.
+__global__ void __launch_bounds__(1024) embed_ln_kernel(int M, int d, const RowDesc* rows,
+                                                       const uint16_t* tok_emb,
+                                                       const uint16_t* pos_emb, float* x,
+                                                       const float* in_rows, const uint16_t* g,
+                                                       const uint16_t* b, uint16_t* frag, int RT) {
+  __shared__ float red_mean[16], red_var[16];
+  const int m = xcd_row(blockIdx.x), j = threadIdx.x * 4;
   if (m >= M) return;
+  const bool on = j < d;
+  const int jc = on ? j : 0;
+  const float4 gv = ld_bf16x4(g, jc), bv = ld_bf16x4(b, jc);
   const RowDesc r = rows[m];
-  float sum = 0.f;
-  for (int j = threadIdx.x; j < d; j += 256) {
-    const float v = (in_rows ? in_rows[(size_t)m * d + j] : S::ld(tok_emb, (size_t)r.token * d + j)) +
-                    S::ld(pos_emb, (size_t)r.pos * d + j);
-    x[(size_t)m * d + j] = v;
-    row[j] = v;
-    sum += v;
-  }
-  const float mean = block_sum<4>(sum, red) / (float)d;
-  float var = 0.f;
-  for (int j = threadIdx.x; j < d; j += 256) {
-    const float t = row[j] - mean;
-    var += t * t;
-  }
-  const float rstd = 1.0f / sqrtf(block_sum<4>(var, red) / (float)d + 1e-5f);
-  for (int j = threadIdx.x; j < d; j += 256)
-    afrag_store(frag, RT, m, j, (row[j] - mean) * rstd * S::ld(g, j) + S::ld(b, j));
+  const float4 te = in_rows ? *(const float4*)(in_rows + (size_t)m * d + jc)
+                            : ld_bf16x4(tok_emb + (size_t)r.token * d, jc);
+  const float4 pe = ld_bf16x4(pos_emb + (size_t)r.pos * d, jc);
+  const float4 v{te.x + pe.x, te.y + pe.y, te.z + pe.z, te.w + pe.w};
+  if (on) *(float4*)(x + (size_t)m * d + j) = v;
+  const float mean = row_block_sum_once(on ? (v.x + v.y) + (v.z + v.w) : 0.f, red_mean) / (float)d;
+  const float4 c{v.x - mean, v.y - mean, v.z - mean, v.w - mean};
+  const float var = row_block_sum_once(on ? (c.x * c.x + c.y * c.y) + (c.z * c.z + c.w * c.w) : 0.f, red_var);
+  const float rstd = 1.0f / sqrtf(var / (float)d + 1e-5f);
+  if (on)
+    afrag_store4(frag, RT, m, j,
+                 float4{c.x * rstd * gv.x + bv.x, c.y * rstd * gv.y + bv.y, c.z * rstd * gv.z + bv.z,
+                        c.w * rstd * gv.w + bv.w});
 }
 
 __global__ void zero_i32_kernel(int* p, int n) {
@@ -571,7 +568,8 @@ void launch_reduce_res_ln(int M, int d, int nsplit, const float* P, const void* 
 void launch_embed_ln(int M, int d, const RowDesc* rows, const void* tok, const void* pos, float* x,
                      const float* in_rows, const void* g, const void* b, uint16_t* frag, int RT,
                      hipStream_t st) {
-  hipLaunchKernelGGL(embed_ln_kernel<BF16>, dim3(xcd_row_grid(M)), dim3(256), d * sizeof(float), st, M, d, rows,
+  const int threads = (d / 4 + kWave - 1) / kWave * kWave;
+  hipLaunchKernelGGL(embed_ln_kernel, dim3(xcd_row_grid(M)), dim3(threads), 0, st, M, d, rows,
                      (const uint16_t*)tok, (const uint16_t*)pos, x, in_rows, (const uint16_t*)g,
                      (const uint16_t*)b, frag, RT);
 }

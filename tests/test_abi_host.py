@@ -152,6 +152,8 @@ def test_verify_step_rejects_before_enqueue(ad):
     assert b"workspace" in ad.LIB.ad_last_error()
     assert run(_step(ad, workspace=0x1010)) == -1                   # misaligned workspace
     assert b"aligned" in ad.LIB.ad_last_error()
+    assert run(_step(ad, in_rows=0x1004)) == -1                     # misaligned input rows
+    assert b"aligned" in ad.LIB.ad_last_error()
     assert ad.LIB.ad_kv_commit(None, None, 2, None) == -1
     assert ad.LIB.ad_kv_commit(0x1000, 0x1000, 0, None) == -2
     kv = ad.KV(0x1000, 56, 28, 0x1000, 0x1000)
