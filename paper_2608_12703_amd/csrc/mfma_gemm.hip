@@ -440,6 +440,142 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
     }
 }
 
+// LM head (argmax epilogue, unsplit) with 16 row tiles and 256 columns per workgroup:
+// at the verify block's 224 rows the 406 column tiles of the vocabulary then fit one
+// round of 203 workgroups (128 columns per workgroup take two rounds).  Eight waves, each
+// with 4 row tiles x 8 column tiles; both operands through three-stage LDS rings filled
+// by direct loads two steps ahead (144 KB).  Every output's sums run in the same order
+// as in gemm_mfma_kernel, and the per-64-column top-2 records land in the same slots.
+template <bool PACKED>
+__global__ void __launch_bounds__(512) lm_head_kernel(GemmArgs g) {
+  constexpr int RTC = 16, RW = 4, CT = 8, NA = RTC / 4;
+  __shared__ uint4 sa0[RTC * 128], sa1[RTC * 128], sa2[RTC * 128];
+  __shared__ uint4 sw0[2 * 512], sw1[2 * 512], sw2[2 * 512];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int rg = w & 3, ch = w >> 2;   // row group (4 row tiles), 128-column half
+  const int c16 = lane & 15, grp = lane >> 4;
+
+  // (column group of 256, row chunk), numbered so each XCD holds a contiguous id range
+  const int nwg = gridDim.x, bid = blockIdx.x;
+  const int x = bid & 7, q8 = nwg >> 3, r8 = nwg & 7;
+  const int lin = x * q8 + min(x, r8) + (bid >> 3);
+  const int mc = lin % g.mchunks, nt = lin / g.mchunks;
+  const int rt0 = mc * RTC, n0 = nt * 2 * kNT;
+
+  f32x4 acc[RW][CT];
+#pragma unroll
+  for (int r = 0; r < RW; ++r)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int kl = g.KB - 1;
+  auto ia = [&](uint4* buf, int kb) {   // activation stage of step kb (clamped)
+    const uint4* src = (const uint4*)g.A + ((size_t)min(kb, kl) * g.RT + rt0) * 128;
+#pragma unroll
+    for (int ii = 0; ii < NA; ++ii) {
+      const int i = ii * 8 + w;
+      dma16(src + i * 64 + lane, buf + i * 64);
+    }
+  };
+  auto iw = [&](uint4* buf, int kb) {   // weight stage of step kb (clamped): two column tiles
+    const int k = min(kb, kl);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if constexpr (PACKED) {
+        const int t = min(nt * 2 + h, g.ntiles - 1);
+        dma16(g.W + ((size_t)(t * g.KB + k) * 512 + w * 64 + lane) * 8, buf + h * 512 + w * 64);
+      } else {
+        const int n = min(n0 + h * kNT + w * 16 + (lane & 15), g.N - 1);
+        dma16(g.W + (size_t)n * g.K + k * 32 + (lane >> 4) * 8, buf + h * 512 + w * 64);
+      }
+    }
+  };
+  auto mma = [&](const uint4* abuf, const uint4* wbuf) __attribute__((always_inline)) {
+    bf16x8 b[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) b[ct] = as_bf16x8(wbuf[ch * 512 + ct * 64 + lane]);
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      const int rt = rg * RW + r;
+      const bf16x8 ah = as_bf16x8(abuf[(rt * 2 + 0) * 64 + lane]);
+      const bf16x8 al = as_bf16x8(abuf[(rt * 2 + 1) * 64 + lane]);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        acc[r][ct] = mfma_bf16(ah, b[ct], acc[r][ct]);
+        acc[r][ct] = mfma_bf16(al, b[ct], acc[r][ct]);
+      }
+    }
+  };
+  // Step j requests A(j + 2) then W(j + 2) into the stages step j - 1 read; at the end of
+  // step j the loads issued after W(j + 1) are A(j + 2) and W(j + 2).
+  constexpr int kWait = NA + 2;
+  ia(sa0, 0);
+  iw(sw0, 0);
+  ia(sa1, 1);
+  iw(sw1, 1);
+  BARRIER_VMCNT(kWait);
+  int kb = 0;
+#define LM_STEP(CA, CW, NXA, NXW) \
+  {                               \
+    ia(NXA, kb + 2);              \
+    iw(NXW, kb + 2);              \
+    mma(CA, CW);                  \
+    BARRIER_VMCNT(kWait);         \
+    ++kb;                         \
+  }
+  for (int it = 0; it < g.KB / 3; ++it) {
+    LM_STEP(sa0, sw0, sa2, sw2)
+    LM_STEP(sa1, sw1, sa0, sw0)
+    LM_STEP(sa2, sw2, sa1, sw1)
+  }
+  const int rem = g.KB % 3;
+  if (rem >= 1) LM_STEP(sa0, sw0, sa2, sw2)
+  if (rem >= 2) LM_STEP(sa1, sw1, sa0, sw0)
+#undef LM_STEP
+  BARRIER_VMCNT(0);
+
+  // top-2 of each 64-column half of this wave's 128 columns per row, stored in the slot
+  // of that 64-column block (the slots gemm_mfma_kernel uses)
+  const int row_base = (rt0 + rg * RW) * 16 + grp * 4;   // + r * 16 + i
+  const int col_base = n0 + ch * kNT + c16;              // + ct * 16
+#pragma unroll
+  for (int r = 0; r < RW; ++r)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = row_base + r * 16 + i;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        Top2s t{-INFINITY, 0x7fffffff, -INFINITY, 0};
+#pragma unroll
+        for (int ct = 4 * q; ct < 4 * q + 4; ++ct) {
+          const int n = col_base + ct * 16;
+          const float v = acc[r][ct][i];
+          const bool fin = isfinite(v), in = n < g.N;
+          const Top2s u{(in & fin) ? v : -INFINITY, in ? n : 0x7fffffff, -INFINITY,
+                        (in & !fin) ? 1 : 0};
+          t = t2_merge(t, u);
+        }
+        t = t2_row16(t);
+        const int slot = nt * 4 + ch * 2 + q;
+        if (c16 == 0 && m < g.M && slot < 2 * g.ntiles) {
+          float4 rec{t.v1, __int_as_float(t.i1), t.v2, __int_as_float(t.bad)};
+          ((float4*)g.e.am_part)[(size_t)m * (2 * g.ntiles) + slot] = rec;
+        }
+      }
+    }
+  if (g.e.out) {
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = row_base + r * 16 + i, n = col_base + ct * 16;
+          if (m < g.M && n < g.N) g.e.out[(size_t)m * g.e.ldo + n] = acc[r][ct][i];
+        }
+  }
+}
+
 // Tiled weight copy (see launch.h): one thread per 16-byte piece.
 __global__ void __launch_bounds__(256) pack_weight_kernel(const uint16_t* W, int N, int K,
                                                           uint16_t* P, size_t pieces) {
@@ -560,6 +696,13 @@ template <int EPI>
 static void launch_one(GemmArgs g, hipStream_t st) {
   const int rtc = gemm_rtc(g.M, g.N, g.S);
   g.mchunks = mchunks_of(g.M, rtc);
+  if (EPI == EPI_ARGMAX && rtc == 16 && g.ntiles * g.mchunks > kMaxWGs &&
+      (g.ntiles + 1) / 2 * g.mchunks <= kMaxWGs) {
+    const dim3 grid((g.ntiles + 1) / 2 * g.mchunks);
+    if (g.packed) hipLaunchKernelGGL(lm_head_kernel<true>, grid, dim3(512), 0, st, g);
+    else hipLaunchKernelGGL(lm_head_kernel<false>, grid, dim3(512), 0, st, g);
+    return;
+  }
   const dim3 grid(g.ntiles * g.S * g.mchunks);
   if (g.packed) {
     if (rtc == 4) launch_rtc<EPI, 4, true>(g, grid, st);
