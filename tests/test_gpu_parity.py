@@ -193,3 +193,41 @@ def test_tiled_weights_are_bit_identical():
         out.append(sess.results())
     for key in ("accept_len", "out_tokens", "greedy", "logits", "hidden"):
         np.testing.assert_array_equal(out[0][key], out[1][key])
+
+
+def test_wide_column_lm_head_matches_oracle_and_row_major_weights():
+    """The LM head's 256-column workgroups (blocks of more than 8 and up to 16 row tiles
+    whose vocabulary has more than 256 column tiles): 20 sequences x 8 rows = 160 rows,
+    vocab 40000 (313 column tiles, an odd count: the last workgroup's second tile lies
+    past the vocabulary).  Tiled and row-major weights agree bit for bit, the logits and
+    greedy tokens of planted sequences match the oracle, and each sequence's first row
+    is bit-equal to its row in a one-row-per-sequence step (the 4-row-tile product)."""
+    cfg = UNIT.with_(vocab=40000, batch=20, k=7, k_min=7, seed=11)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    planted = {0, 7, 19}
+    blocks, _ = planted_blocks(cfg, model, wl, planted)
+    out = []
+    for pack in (True, False):
+        sess = device_session(cfg, params, wl, want_logits=True)
+        if not pack:
+            sess.model.pack(None)
+        sess.step(blocks)
+        out.append((sess, sess.results()))
+    (sess, res), (_, res_rm) = out
+    assert res["err"] == 0
+    for key in ("accept_len", "out_tokens", "greedy", "logits", "hidden", "margin"):
+        np.testing.assert_array_equal(res[key], res_rm[key], err_msg=key)
+    taps = step_taps(sess, blocks)
+    for b in sorted(planted):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+        compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
+    # the same pending tokens as a one-row block per sequence (20 rows: 4-row tiles)
+    one = device_session(cfg, params, wl, want_logits=True, k_max=0)
+    one.step([np.array(blocks[b][:1], np.int64) for b in range(wl.batch)])
+    r1 = one.results()
+    rows = [sess.row_of(b, 0) for b in range(wl.batch)]
+    np.testing.assert_array_equal(r1["logits"].view(np.uint32), res["logits"][rows].view(np.uint32))
+    np.testing.assert_array_equal(r1["greedy"], res["greedy"][rows])
