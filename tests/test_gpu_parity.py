@@ -231,3 +231,33 @@ def test_wide_column_lm_head_matches_oracle_and_row_major_weights():
     rows = [sess.row_of(b, 0) for b in range(wl.batch)]
     np.testing.assert_array_equal(r1["logits"].view(np.uint32), res["logits"][rows].view(np.uint32))
     np.testing.assert_array_equal(r1["greedy"], res["greedy"][rows])
+
+
+@pytest.mark.parametrize("batch", [80, 160])
+def test_up_projection_epilogue_at_wide_and_16_row_tiles(batch):
+    """FFN-up's bias + GELU epilogue in the layouts large blocks take: d_ffn 5120 (40
+    column tiles) at 640 rows runs 8-row-tile workgroups (the wide layout) and at 1280
+    rows 16-row-tile workgroups.  Every sequence's first row is bit-equal to its row in a
+    one-row-per-sequence step (4-row tiles), and planted sequences match the oracle."""
+    cfg = UNIT.with_(d_ffn=5120, batch=batch, k=7, k_min=7, seed=13)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    planted = {0, batch - 1}
+    blocks, _ = planted_blocks(cfg, model, wl, planted)
+    sess = device_session(cfg, params, wl, want_logits=True)
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    taps = step_taps(sess, blocks)
+    for b in sorted(planted):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+        compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
+    one = device_session(cfg, params, wl, want_logits=True, k_max=0)
+    one.step([np.array(blocks[b][:1], np.int64) for b in range(wl.batch)])
+    r1 = one.results()
+    rows = [sess.row_of(b, 0) for b in range(wl.batch)]
+    for key in ("logits", "hidden"):
+        np.testing.assert_array_equal(r1[key].view(np.uint32), res[key][rows].view(np.uint32), err_msg=key)
+    np.testing.assert_array_equal(r1["greedy"], res["greedy"][rows])
