@@ -48,7 +48,7 @@ def decode_with_heads(sess, heads_w, t0, n_tokens: int):
         sess.commit()
         ad.draft_heads(sess.model, heads_w, H, sess.out_hidden, sess.layout, sess.k_max, None,
                        sess.accept_len, sess.out_tokens, B, nxt, ws)
-        res = sess.results()
+        res = sess.results(keys=("accept_len", "out_tokens", "err"))
         assert res["err"] == 0, f"device error flag {res['err']}"
         a = res["accept_len"]
         accepts.append(a.copy())
@@ -90,7 +90,7 @@ def decode_with_drift(sess, ys, plans, k: int, n_tokens: int, ks_out=None):
                   for b in range(B)]
         sess.step(blocks)
         sess.commit()
-        res = sess.results()
+        res = sess.results(keys=("accept_len", "out_tokens", "err"))
         assert res["err"] == 0, f"device error flag {res['err']}"
         a = res["accept_len"]
         accepts.append(a.copy())
@@ -198,7 +198,7 @@ def decode_with_draft(target, runner: DraftRunner, t0, K: int, n_tokens: int, an
         target.step(blocks)
         target.commit()
         nxt = runner.round(K).cpu().numpy()
-        res = target.results()
+        res = target.results(keys=("accept_len", "out_tokens", "err"))
         assert res["err"] == 0, f"device error flag {res['err']}"
         a = res["accept_len"]
         accepts.append(a.copy())

@@ -207,8 +207,17 @@ class Session:
             return b * (self.k_max + 1) + i
         return int(self.cu_rows[b].item()) + i
 
-    def results(self) -> dict:
+    def results(self, keys=None) -> dict:
+        """The step's outputs on the host; keys limits the copies to the named ones (a
+        decode loop needs only accept_len, out_tokens and err)."""
         torch.cuda.synchronize()
+        if keys is not None:
+            src = {"accept_len": self.accept_len, "out_tokens": self.out_tokens,
+                   "kv_len": self.kv_len, "greedy": self.out_greedy[: self.rows]}
+            out = {k: src[k].cpu().numpy() for k in keys if k != "err"}
+            if "err" in keys:
+                out["err"] = int(self.err_flag.item())
+            return out
         out = {"accept_len": self.accept_len.cpu().numpy(),
                "out_tokens": self.out_tokens.cpu().numpy(),
                "greedy": self.out_greedy[: self.rows].cpu().numpy(),
