@@ -261,3 +261,31 @@ def test_up_projection_epilogue_at_wide_and_16_row_tiles(batch):
     for key in ("logits", "hidden"):
         np.testing.assert_array_equal(r1[key].view(np.uint32), res[key][rows].view(np.uint32), err_msg=key)
     np.testing.assert_array_equal(r1["greedy"], res["greedy"][rows])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_longest_block_64_rows(dtype):
+    """The largest block a sequence may verify: 64 rows (k = 63; the row masks use all 64
+    bits, four 16-row query groups), next to a one-row block, with drafts planted on the
+    oracle's continuation so acceptance runs deep; the last block ends at the last
+    position."""
+    cfg = UNIT.with_(dtype=dtype, batch=3, k=63, k_min=63, geo_p=0.02, seed=17)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    wl.n[2] = MAX_POS - 64
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, {0, 2})
+    blocks[1] = blocks[1][:1]
+    wl.k[1] = 0
+    sess = device_session(cfg, params, wl, k_max=63)
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    taps = step_taps(sess, blocks)
+    for b in range(wl.batch):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+        compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
+    sess.commit()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sess.kv_len.cpu().numpy(), wl.n + res["accept_len"] + 1)
