@@ -138,10 +138,10 @@ def param_count(cfg) -> int:
 class Model:
     """A model handle over caller-owned device parameters (kept alive here)."""
 
-    def __init__(self, cfg, params: list):
+    def __init__(self, cfg, params: list, max_frames: int = 1500):
         self.cfg = cfg
         self.params = params
-        self.desc = model_desc(cfg)
+        self.desc = model_desc(cfg, max_frames=max_frames)
         arr = (_ptr * len(params))(*[p.data_ptr() for p in params])
         h = _ptr()
         check(LIB.ad_model_create(ctypes.byref(self.desc), arr, len(params), ctypes.byref(h)),

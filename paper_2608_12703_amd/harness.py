@@ -38,13 +38,13 @@ class Session:
     def __init__(self, cfg: Config, params, batch: int, k_max: int, frames, *,
                  layout: int = ad.AD_PADDED, packed_encoder: bool = False,
                  page_seed: int | None = 0, want_logits: bool = False, device: str = "cuda",
-                 extra_pages: int = 0, pack_weights: bool = True):
+                 extra_pages: int = 0, pack_weights: bool = True, max_frames: int = MAX_FRAMES):
         self.cfg, self.B, self.k_max, self.layout = cfg, batch, k_max, layout
         self.device = device
         self.dt = torch_dtype(cfg)
         L, d, H = cfg.n_layers, cfg.d_model, cfg.n_heads
         self.params = params if isinstance(params, list) else upload_params(cfg, params, device)
-        self.model = ad.Model(cfg, self.params)
+        self.model = ad.Model(cfg, self.params, max_frames=max_frames)
         if pack_weights and cfg.dtype == "bf16":   # tiled weights for the matrix-core GEMMs
             self.model.pack(torch.empty(self.model.pack_size(), dtype=torch.uint8, device=device))
         i32 = dict(dtype=torch.int32, device=device)
@@ -62,7 +62,7 @@ class Session:
 
         # encoder K/V slots
         frames = [int(t) for t in frames]
-        assert len(frames) == batch and all(1 <= t <= MAX_FRAMES for t in frames)
+        assert len(frames) == batch and all(1 <= t <= max_frames for t in frames)
         self.frames = frames
         if packed_encoder:
             off = np.concatenate([[0], np.cumsum([_ceil32(t) for t in frames])])

@@ -38,12 +38,12 @@ def subset(wl, ids):
 
 
 def device_session(cfg, params, wl, *, layout=ad.AD_PADDED, packed_encoder=False,
-                   want_logits=True, poison=False, k_max=None, seq_ids=None):
+                   want_logits=True, poison=False, k_max=None, seq_ids=None, max_frames=1500):
     """Device state for workload `wl`; sequence b draws the inputs of seq_ids[b]."""
     k_max = int(wl.k.max()) if k_max is None else k_max
     ids = list(range(wl.batch)) if seq_ids is None else list(seq_ids)
     s = Session(cfg, params, wl.batch, k_max, wl.T, layout=layout,
-                packed_encoder=packed_encoder, want_logits=want_logits)
+                packed_encoder=packed_encoder, want_logits=want_logits, max_frames=max_frames)
     if poison:
         s.pool.fill_(float("nan"))
         s.cross.fill_(float("nan"))

@@ -289,3 +289,26 @@ def test_longest_block_64_rows(dtype):
     sess.commit()
     torch.cuda.synchronize()
     np.testing.assert_array_equal(sess.kv_len.cpu().numpy(), wl.n + res["accept_len"] + 1)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_most_encoder_frames(dtype):
+    """The most encoder frames a model may declare (max_frames 2048): six 384-frame
+    chunks per cross-attention workgroup (bf16), sixteen 128-key groups (float32), in the
+    padded and the packed encoder layouts."""
+    cfg = UNIT.with_(dtype=dtype, batch=3, frames=2048, frames_min=2000, seed=19)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    wl.T[0] = 2048
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, set(range(wl.batch)))
+    for packed in (False, True):
+        sess = device_session(cfg, params, wl, packed_encoder=packed, poison=True, max_frames=2048)
+        sess.step(blocks)
+        res = sess.results()
+        assert res["err"] == 0
+        taps = step_taps(sess, blocks)
+        for b in range(wl.batch):
+            st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+            ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+            compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
