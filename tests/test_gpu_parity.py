@@ -312,3 +312,23 @@ def test_most_encoder_frames(dtype):
             st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
             ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
             compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_widest_model(dtype):
+    """The widest model the library takes: 64 heads, d_model 4096 (one thread per four
+    columns fills a 1024-thread row kernel; 64 attention workgroups per sequence)."""
+    cfg = UNIT.with_(dtype=dtype, n_layers=1, d_model=4096, n_heads=64, d_ffn=512, batch=2, k=3, k_min=0,
+                     frames=96, frames_min=1, kv_max=40, seed=23)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, set(range(wl.batch)))
+    sess = device_session(cfg, params, wl)
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    for b in range(wl.batch):   # one layer: its cache values take the first layer's bar
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:])
+        compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]))
