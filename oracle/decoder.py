@@ -32,7 +32,7 @@ from .numerics import round_f32, store
 
 HEAD = 64
 EPS = 1e-5
-MAX_POS = 448
+MAX_POS = 448   # rows of the Whisper-shape position table (a model may carry another)
 
 
 # ---------------------------------------------------------------------- sublayers
@@ -91,6 +91,8 @@ class Model:
         self.F, self.V = cfg.d_ffn, cfg.vocab
         self.params = params
         self.kv_dtype = kv_dtype or cfg.dtype
+        # decoder positions: the rows of the learned position table
+        self.max_pos = len(params["pos_emb"])
 
     def w(self, name):
         return np.asarray(self.params[name], dtype=np.float64)
@@ -188,7 +190,7 @@ def forward_block(model: Model, state: SeqState, tokens, probe_layer: int | None
     sits at position n + depth(i) and attends to the committed keys and its ancestors."""
     tokens = np.asarray(tokens, dtype=np.int64)
     r, n, d, H = len(tokens), state.n, model.d, model.H
-    if n + r > MAX_POS:
+    if n + r > model.max_pos:
         raise ValueError("block runs past the last decoder position")
     pos = n + (np.arange(r) if parents is None else np.asarray(tree_depths(parents)))
     self_vis = pos + 1 if parents is None else tree_visibility(parents, n)
@@ -302,7 +304,7 @@ def spec_decode_heads(model: Model, state: SeqState, heads_w, n_tokens: int):
     toks += r.emitted
     hidden, state = r.hidden[r.accepted], r.state
     while len(toks) < n_tokens:
-        k = min(len(heads_w), MAX_POS - 1 - state.n)
+        k = min(len(heads_w), model.max_pos - 1 - state.n)
         drafts = draft_heads(heads_w[:k], hidden)
         r = verify(model, state, drafts)
         rounds.append(r)

@@ -141,7 +141,7 @@ class Model:
     def __init__(self, cfg, params: list, max_frames: int = 1500):
         self.cfg = cfg
         self.params = params
-        self.desc = model_desc(cfg, max_frames=max_frames)
+        self.desc = model_desc(cfg, max_pos=cfg.max_pos, max_frames=max_frames)
         arr = (_ptr * len(params))(*[p.data_ptr() for p in params])
         h = _ptr()
         check(LIB.ad_model_create(ctypes.byref(self.desc), arr, len(params), ctypes.byref(h)),

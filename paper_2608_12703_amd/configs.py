@@ -39,6 +39,7 @@ class Config:
     decode_tokens: int = 0      # loop configs: tokens to decode
     draft_heads: int = 0        # linear draft heads on the final hidden state
     anchor_lambda: float = 0.0  # drift stress: Poisson gap between misalignment anchors
+    max_pos: int = MAX_POS      # decoder positions (rows of the learned position table)
     seed: int = 0
     notes: str = ""
 
@@ -53,7 +54,7 @@ class Config:
         d, F, L, V = self.d_model, self.d_ffn, self.n_layers, self.vocab
         per_layer = 3 * d * d + 3 * d + d * d + d + d * d + d + 2 * d * d + 2 * d \
             + d * d + d + F * d + F + d * F + d + 6 * d
-        return L * per_layer + V * d + MAX_POS * d + 2 * d
+        return L * per_layer + V * d + self.max_pos * d + 2 * d
 
 
 TINY_FP32 = Config(

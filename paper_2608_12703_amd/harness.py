@@ -50,7 +50,7 @@ class Session:
         i32 = dict(dtype=torch.int32, device=device)
 
         # paged self-KV: every sequence may reach the last position
-        self.pages_per_seq = (MAX_POS + PAGE - 1) // PAGE
+        self.pages_per_seq = (cfg.max_pos + PAGE - 1) // PAGE
         self.num_pages = batch * self.pages_per_seq + extra_pages
         order = np.arange(self.num_pages)
         if page_seed is not None:

@@ -68,7 +68,7 @@ def param_specs(cfg: Config):
     Matrices are stored [out_features, in_features] row-major.
     """
     d, F, V = cfg.d_model, cfg.d_ffn, cfg.vocab
-    shapes = {"tok_emb": (V, d), "pos_emb": (MAX_POS, d), "lnf_g": (d,), "lnf_b": (d,),
+    shapes = {"tok_emb": (V, d), "pos_emb": (cfg.max_pos, d), "lnf_g": (d,), "lnf_b": (d,),
               "ln1_g": (d,), "ln1_b": (d,), "w_qkv": (3 * d, d), "b_qkv": (3 * d,),
               "w_o": (d, d), "b_o": (d,), "ln2_g": (d,), "ln2_b": (d,),
               "w_xq": (d, d), "b_xq": (d,), "w_xkv": (2 * d, d), "b_xkv": (2 * d,),
@@ -202,7 +202,7 @@ def make_step_workload(cfg: Config, seed: int | None = None, batch: int | None =
         gs = _rng(seed, S_SHAPE, b)
         k[b] = cfg.k if cfg.k_min < 0 else gs.integers(cfg.k_min, cfg.k + 1)
         T[b] = cfg.frames if cfg.frames_min < 0 else gs.integers(cfg.frames_min, cfg.frames + 1)
-        kv_hi = min(cfg.kv_max, MAX_POS - 1 - int(k[b]))
+        kv_hi = min(cfg.kv_max, cfg.max_pos - 1 - int(k[b]))
         n[b] = _rng(seed, S_KVLEN, b).integers(0, kv_hi + 1)
         gp = _rng(seed, S_GEO, b)
         G[b] = (gp.geometric(cfg.geo_p) - 1) if cfg.geo_p > 0 else 0

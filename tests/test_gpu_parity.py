@@ -332,3 +332,26 @@ def test_widest_model(dtype):
         st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
         ref = od.verify(model, st, blocks[b][1:])
         compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_most_decoder_positions(dtype):
+    """The most decoder positions a model may declare (max_pos 1024: eight 128-key chunks
+    per self-attention workgroup), committed prefixes up to 1018 tokens, one block ending
+    at the last position."""
+    cfg = UNIT.with_(dtype=dtype, max_pos=1024, batch=3, k=5, k_min=0, kv_max=1018, seed=29)
+    params = synth.make_params(cfg)
+    wl = synth.make_step_workload(cfg)
+    wl.n[2] = cfg.max_pos - 1 - int(wl.k[2])
+    model = oracle_model(cfg, params)
+    blocks, _ = planted_blocks(cfg, model, wl, set(range(wl.batch)))
+    sess = device_session(cfg, params, wl, poison=True)
+    sess.step(blocks)
+    res = sess.results()
+    assert res["err"] == 0
+    taps = step_taps(sess, blocks)
+    for b in range(wl.batch):
+        st = oracle_state(cfg, model, b, int(wl.n[b]), int(wl.T[b]), int(wl.t0[b]))
+        ref = od.verify(model, st, blocks[b][1:], taps=list(range(cfg.n_layers - 1)))
+        compare_sequence(cfg, sess, res, b, blocks[b], ref, int(wl.n[b]), gpu_taps=taps)
+    print("committed lengths", wl.n.tolist(), "blocks", [len(x) for x in blocks])
