@@ -6,11 +6,11 @@
 // other's matrix instructions) each own a quarter of the rows and half of the columns
 // (with 8 row tiles: one row tile and all the columns each).
 // Weights (streamed from HBM) move in 32-wide K steps through an LDS ring filled by
-// direct global->LDS loads five steps ahead.  Activations (L2-resident) go straight into
-// a register ring five steps ahead for tiles of up to 8 row tiles (the A-fragment order
-// is the matrix instruction's lane order, so each is one coalesced 16-byte load per
-// lane; keeping them out of LDS removes a third of the step's LDS traffic), and through
-// a three-stage LDS ring for 16 row tiles.  Workgroups with long K ranges (the FFN
+// direct global->LDS loads three to five steps ahead.  Activations (L2-resident) go
+// straight into a register ring as far ahead for tiles of up to 8 row tiles (the
+// A-fragment order is the matrix instruction's lane order, so each is one coalesced
+// 16-byte load per lane; keeping them out of LDS removes a third of the step's LDS
+// traffic), and through a three-stage LDS ring for 16 row tiles.  Workgroups with long K ranges (the FFN
 // products) take two K steps per barrier.  The waits are explicit; the loops are unrolled
 // over the ring stages so every buffer is a distinct object.  Small-N products split K
 // over several workgroups, each storing its raw partial tile; the kernel that consumes
@@ -211,13 +211,12 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
   int kb = kb0;
   if constexpr (RTC <= 8) {
     // Activations straight into registers (the A-fragment layout is the matrix
-    // instruction's lane order, so each is one coalesced 16-byte load per lane), five
-    // steps ahead like the weights: only the weights pass through LDS, which halves the
-    // LDS traffic of a step.  Step j requests A(j+5) then W(j+5); at the end of step j
-    // the loads issued after W(j+1) are four (A, W) pairs, so the barrier's wait also
-    // completes A(j+1) and the compiler needs no wait of its own for the registers.
+    // instruction's lane order, so each is one coalesced 16-byte load per lane), as far
+    // ahead as the weights: only the weights pass through LDS, which halves the LDS
+    // traffic of a step.  A step requests A then W; the barrier's wait counts whole
+    // (A, W) pairs, so it also completes the activations of the next step and the
+    // compiler needs no wait of its own for the registers.
     constexpr int kA = 2 * RW;                       // activation loads per step
-    constexpr int kWait = 4 * (kA + 1);
     const uint4* abase = (const uint4*)g.A + ((size_t)rt0 + rg * RW) * 128 + lane;
     auto la = [&](AFrag<RW>& f, int k) {
       const uint4* src = abase + (size_t)min(k, kl) * g.RT * 128;
@@ -265,39 +264,36 @@ __global__ void __launch_bounds__(512) gemm_mfma_kernel(GemmArgs g) {
       if (rem >= 2) GEMM_ITER(a2, sw2, a3, sw3, a0, sw0, a1, sw1)
 #undef GEMM_ITER
     } else {
+      // One step per barrier, operands three steps ahead (four ring slots): step j
+      // requests A(j+3) then W(j+3) into the slots step j - 1 read and ends with step
+      // j + 1 complete (two steps' loads still in flight).  (Five steps ahead measured
+      // 0.16 us slower per launch in the verify step, two steps ahead slower still.)
+      constexpr int kWait1 = 2 * (kA + 1);
       la(a0, kb0);
       iw(sw0, kb0);
       la(a1, kb0 + 1);
       iw(sw1, kb0 + 1);
       la(a2, kb0 + 2);
       iw(sw2, kb0 + 2);
-      la(a3, kb0 + 3);
-      iw(sw3, kb0 + 3);
-      la(a4, kb0 + 4);
-      iw(sw4, kb0 + 4);
-      BARRIER_VMCNT(kWait);
-#define GEMM_STEP(CA, CW, NXA, NXW)                 \
-    {                                               \
-      la(NXA, kb + 5);                              \
-      iw(NXW, kb + 5);                              \
+      BARRIER_VMCNT(kWait1);
+#define GEMM_STEP(CA, CW, NXA, NXW)                      \
+    {                                                    \
+      la(NXA, kb + 3);                                   \
+      iw(NXW, kb + 3);                                   \
       mma_step_reg<RW, CT, kSw>(acc, CA, CW, ch, lane);  \
-      BARRIER_VMCNT(kWait);                         \
-      ++kb;                                         \
+      BARRIER_VMCNT(kWait1);                             \
+      ++kb;                                              \
     }
-      for (int it = 0; it < nk / 6; ++it) {
-        GEMM_STEP(a0, sw0, a5, sw5)
+      for (int it = 0; it < nk / 4; ++it) {
+        GEMM_STEP(a0, sw0, a3, sw3)
         GEMM_STEP(a1, sw1, a0, sw0)
         GEMM_STEP(a2, sw2, a1, sw1)
         GEMM_STEP(a3, sw3, a2, sw2)
-        GEMM_STEP(a4, sw4, a3, sw3)
-        GEMM_STEP(a5, sw5, a4, sw4)
       }
-      const int rem = nk % 6;
-      if (rem >= 1) GEMM_STEP(a0, sw0, a5, sw5)
+      const int rem = nk % 4;
+      if (rem >= 1) GEMM_STEP(a0, sw0, a3, sw3)
       if (rem >= 2) GEMM_STEP(a1, sw1, a0, sw0)
       if (rem >= 3) GEMM_STEP(a2, sw2, a1, sw1)
-      if (rem >= 4) GEMM_STEP(a3, sw3, a2, sw2)
-      if (rem >= 5) GEMM_STEP(a4, sw4, a3, sw3)
 #undef GEMM_STEP
     }
   } else {
