@@ -637,17 +637,18 @@ int gemm_splits(int N, int K) {
   return best_s;
 }
 
-// Row tiles per workgroup: the smallest tile whose grid stays within 1.5 workgroups per
+// Row tiles per workgroup: the smallest tile whose grid stays within one workgroup per
 // CU (the activation buffer holds a multiple of 16 row tiles, so every staged block lies
-// in it).  For larger blocks, 4-row-tile workgroups sharing some CUs beat 8-row-tile
-// ones in one round (a K step of 8 row tiles costs 0.43 us against 0.27 us): the 352-row
-// block of an 11-node tree at batch 32 takes 6.16 ms per step against 6.58 ms.  The
+// in it).  With the wide 8-row-tile layout (twice the matrix work per K step for the
+// same operand bytes) one round of 8-row-tile workgroups beats 4-row-tile ones sharing
+// CUs: the 352-row block of an 11-node tree at batch 32 takes 5.31 ms per step against
+// 5.86 ms with up to 1.5 four-row-tile workgroups per CU, the ragged 64-sequence batch
+// 6.29 (packed) / 7.22 (padded) against 6.52 / 7.41 ms, the verify step unchanged.  The
 // row tiling never changes a row's sums (same K order, same split order).
 // When no tile fits (the LM head's 406 column tiles), 16 row tiles, or 4 when that
 // needs no more row chunks (up to 64 rows, the draft block's 32): a 4-row-tile K step
-// costs a third of a 16-row-tile one (draft step 198 -> 156 us at batch 32).  For the
-// 352-row tree block 8 row tiles measured slower than 16 (6.20 against 6.16 ms).
-constexpr int kMaxWGsRows = 384;
+// costs a third of a 16-row-tile one (draft step 198 -> 156 us at batch 32).
+constexpr int kMaxWGsRows = 256;
 int gemm_rtc(int M, int N, int S) {
   const int ntiles = (N + kNT - 1) / kNT;
   for (int rtc : {4, 8})
