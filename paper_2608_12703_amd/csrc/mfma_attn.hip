@@ -437,23 +437,35 @@ attn_mfma_kernel(AttnArgs a) {
         // a block's key registers are free once its scores are in: the keys of the block
         // two ahead are requested then, and its values after the value product, so more
         // bytes stay in flight while the softmax runs
-        auto step = [&](KVTiles& t, int blk) __attribute__((always_inline)) {
+        // (pf: request the block two ahead; the last two blocks of the chunk request none)
+        auto step = [&](KVTiles& t, int blk, bool pf) __attribute__((always_inline)) {
           const uint16_t* np = cross_block(a, s, h, blk + 64, k_beg, k_end, c16, grp);
           float sv[8];
           if (blk + 32 <= clean && blk >= k_lo) {
             block_scores<false, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, sv, srow);
-            load_keys(np, t);
+            if (pf) load_keys(np, t);
             block_softmax_pv<false>(t, sv, blk, k_end, grp, o, m_run, l_run);
           } else {
             block_scores<true, SCORES>(t, blk, k_lo, k_end, n0, tmask, grp, qh, ql, sv, srow);
-            load_keys(np, t);
+            if (pf) load_keys(np, t);
             block_softmax_pv<true>(t, sv, blk, k_end, grp, o, m_run, l_run);
           }
-          load_values(np, t);
+          if (pf) load_values(np, t);
         };
-        for (int blk = k_beg; blk < k_end; blk += 64) {
-          step(ta, blk);
-          step(tb, blk + 32);
+        int blk = k_beg;
+        for (; blk + 96 < k_end; blk += 64) {
+          step(ta, blk, true);
+          step(tb, blk + 32, true);
+        }
+        // one to three blocks left (none for a chunk wholly before the window), the first
+        // two already in ta, tb
+        if (blk + 64 < k_end) {
+          step(ta, blk, true);
+          step(tb, blk + 32, false);
+          step(ta, blk + 64, false);
+        } else if (blk < k_end) {
+          step(ta, blk, false);
+          if (blk + 32 < k_end) step(tb, blk + 32, false);
         }
       } else {
         auto attend = [&](const KVTiles& t, int blk) __attribute__((always_inline)) {
@@ -463,11 +475,24 @@ attn_mfma_kernel(AttnArgs a) {
             attend_block<true>(patch_new_rows(t, blk, s.n, nrows, nk, nvt, c16, grp), blk, k_lo, k_end,
                                n0, tmask, grp, qh, ql, o, m_run, l_run);
         };
-        for (int blk = k_beg; blk < k_end; blk += 64) {
+        // no block past the chunk is requested (cross-attention likewise): a load whose
+        // result is never used still has to land before its registers are reused, a full
+        // round trip at the end
+        int blk = k_beg;
+        for (; blk + 96 < k_end; blk += 64) {
           attend(ta, blk);
           load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
           attend(tb, blk + 32);
           load_block<CROSS>(a, s, h, blk + 96, k_beg, k_end, pg_lane, c16, grp, tb);
+        }
+        // one to three blocks left, the first two already in ta, tb
+        attend(ta, blk);
+        if (blk + 64 < k_end) {
+          load_block<CROSS>(a, s, h, blk + 64, k_beg, k_end, pg_lane, c16, grp, ta);
+          attend(tb, blk + 32);
+          attend(ta, blk + 64);
+        } else if (blk + 32 < k_end) {
+          attend(tb, blk + 32);
         }
       }
     }
