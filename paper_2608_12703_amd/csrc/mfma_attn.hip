@@ -427,8 +427,9 @@ attn_mfma_kernel(AttnArgs a) {
     for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    // ping-pong over 32-key blocks with the other block's loads in flight; a block past
-    // the chunk end is fully masked and leaves the state bit-for-bit unchanged
+    // ping-pong over 32-key blocks with the other block's loads in flight; only blocks
+    // that start inside the chunk are processed (one past its end would be fully masked
+    // and leave the state bit-for-bit unchanged)
     {
       // blocks below `clean` need no masking for any query of the group and (self)
       // hold committed keys only
