@@ -335,6 +335,7 @@ void run_step_mfma(const ad_model* m, const ad_step* s, const Workspace& w, hipS
   at.num_pages = s->kv.num_pages; at.block_table = s->kv.block_table;
   at.pages_per_seq = s->kv.pages_per_seq; at.frames_cap = s->cross.frames_cap;
   at.qgroups = w.qgroups; at.qkv_part = w.gpart; at.rows = M; at.tree = w.tree;
+  at.row_stride = s->layout == AD_PADDED ? s->k_max + 1 : 0;
 
   for (int l = 0; l < D.n_layers; ++l) {
     at.layer = l;

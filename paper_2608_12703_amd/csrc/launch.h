@@ -148,6 +148,9 @@ struct AttnArgs {
   const int* block_table;
   int pages_per_seq, frames_cap;
   int chunk, max_chunks, qgroups;   // max_chunks waves per workgroup (at most 8)
+  // self-attention, padded row layout: rows per sequence (sequence b's rows start at
+  // b * row_stride); 0 when the rows are packed (their start comes from the descriptor)
+  int row_stride;
   float* q_save;   // cross-attention only, may be NULL: the finished queries, [rows][d]
   const RowTree* tree;   // self-attention of a draft-tree block (NULL: causal block)
   // cross-attention at the anchor layer, may be NULL: every query row's scores

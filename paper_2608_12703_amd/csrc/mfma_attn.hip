@@ -256,7 +256,7 @@ __device__ __forceinline__ float4 finish_proj4(const AttnArgs& a, int m, int col
   return v;
 }
 
-template <bool CROSS, bool SCORES>
+template <bool CROSS, bool SCORES, bool PAD = false>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(3)))
 attn_mfma_kernel(AttnArgs a) {
   extern __shared__ float part[];  // [waves][kAttnPart], then the queries [16][64]
@@ -273,9 +273,46 @@ attn_mfma_kernel(AttnArgs a) {
     const int p = min(ch * tiles + (lane < tiles ? lane : 0), a.pages_per_seq - 1);
     pg_spec = a.block_table[(size_t)b * a.pages_per_seq + p];
   }
-  const SeqDesc s = a.seqs[b];
-  if (!s.valid) return;
+  // Prologue loads: this thread's first query item and (self) its first block-row item,
+  // SP split planes each, as straight-line code.  Loads complete in issue order, so
+  // waiting for these later leaves the key loads issued after them in flight.
+  constexpr int SP = CROSS ? 8 : 4;
+  const int S = a.qkv_splits;
+  const size_t plane = (size_t)a.rows * a.qkv_n;
+  const int qr = threadIdx.x >> 4, qj = (threadIdx.x & 15) * 4;        // query item
+  const int kr = threadIdx.x >> 5, kkv = (threadIdx.x >> 4) & 1;       // block-row item
+  const int kcol = a.d + kkv * a.d + h * kHead + qj;
   const int q0 = qg * 16;
+  float4 qp[SP], kp[SP];
+  uint2 qb, kbias;
+  size_t qe = 0, ke = 0;
+  auto request = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < SP; ++u) qp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + qe);
+    qb = *(const uint2*)(a.qkv_bias + h * kHead + qj);
+    if (!CROSS) {
+#pragma unroll
+      for (int u = 0; u < SP; ++u) kp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + ke);
+      kbias = *(const uint2*)(a.qkv_bias + kcol);
+    }
+  };
+  if constexpr (PAD) {
+    // padded rows: sequence b's rows start at b * row_stride, so the partials are
+    // requested before the descriptor arrives (rows clamped to the sequence's own; an
+    // item past the block's rows is loaded but never used)
+    const int r0 = b * a.row_stride;
+    qe = (size_t)(r0 + min(q0 + qr, a.row_stride - 1)) * a.qkv_n + h * kHead + qj;
+    ke = (size_t)(r0 + min(kr, a.row_stride - 1)) * a.qkv_n + kcol;
+    request();
+  }
+  const SeqDesc s = a.seqs[b];
+  if constexpr (PAD) {
+    // keep those requests ahead of the descriptor's use (the early returns below would
+    // otherwise let the compiler sink them past it); the fields used here are read
+    // before this point, so they stay scalar loads
+    asm volatile("" ::"s"(s.row0), "s"(s.k), "s"(s.n), "s"(s.valid) : "memory");
+  }
+  if (!s.valid) return;
   const int nq = min(16, s.k + 1 - q0);
   if (nq <= 0) return;
   if (SCORES && a.best_clear && h == 0 && qg == 0 && threadIdx.x == 0) a.best_clear[b] = 0;
@@ -304,30 +341,16 @@ attn_mfma_kernel(AttnArgs a) {
   uint16_t* nvt = nk + kMaxBlockRows * kHead;
   const int nrows = s.k + 1;
 
-  // Prologue loads go out first, as straight-line code: this thread's first query item
-  // and (self) its first block-row item, SP split planes each.  Loads complete in issue
-  // order, so waiting for these later leaves the key loads issued after them in flight.
-  constexpr int SP = CROSS ? 8 : 4;
-  const int S = a.qkv_splits;
-  const size_t plane = (size_t)a.rows * a.qkv_n;
-  const int qr = threadIdx.x >> 4, qj = (threadIdx.x & 15) * 4;        // query item
   const bool q_on = threadIdx.x < 16 * 16 && qr < nq;
-  const size_t qe = (size_t)(s.row0 + q0 + (q_on ? qr : 0)) * a.qkv_n + h * kHead + qj;
-  const int kr = threadIdx.x >> 5, kkv = (threadIdx.x >> 4) & 1;       // block-row item
   const bool k_on = !CROSS && (int)threadIdx.x < nrows * 32;
-  const int kcol = a.d + kkv * a.d + h * kHead + qj;
-  const size_t ke = (size_t)(s.row0 + (k_on ? kr : 0)) * a.qkv_n + kcol;
-  float4 qp[SP], kp[SP];
-  uint2 qb, kbias;
+  if constexpr (!PAD) {
+    qe = (size_t)(s.row0 + q0 + (q_on ? qr : 0)) * a.qkv_n + h * kHead + qj;
+    ke = (size_t)(s.row0 + (k_on ? kr : 0)) * a.qkv_n + kcol;
+    request();
+  }
   int kpg = 0;   // page of this thread's block-row item
   unsigned long long tmask = 0;   // self: the row mask of this lane's query
-#pragma unroll
-  for (int u = 0; u < SP; ++u) qp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + qe);
-  qb = *(const uint2*)(a.qkv_bias + h * kHead + qj);
   if (!CROSS) {
-#pragma unroll
-    for (int u = 0; u < SP; ++u) kp[u] = *(const float4*)(a.qkv_part + (size_t)min(u, S - 1) * plane + ke);
-    kbias = *(const uint2*)(a.qkv_bias + kcol);
     const int slot = s.n + (k_on ? kr : 0);
     kpg = a.block_table[(size_t)b * a.pages_per_seq + slot / kTile];
     tmask = a.tree[s.row0 + q0 + min(c16, nq - 1)].mask;
@@ -543,6 +566,7 @@ void launch_attn_mfma(const AttnArgs& a, int B, hipStream_t st) {
                      (a.cross ? 0 : 2 * kMaxBlockRows * kHead * sizeof(uint16_t));
   if (a.cross && a.score_out) hipLaunchKernelGGL((attn_mfma_kernel<true, true>), grid, block, lds, st, a);
   else if (a.cross) hipLaunchKernelGGL((attn_mfma_kernel<true, false>), grid, block, lds, st, a);
+  else if (a.row_stride > 0) hipLaunchKernelGGL((attn_mfma_kernel<false, false, true>), grid, block, lds, st, a);
   else hipLaunchKernelGGL((attn_mfma_kernel<false, false>), grid, block, lds, st, a);
 }
 
